@@ -1,0 +1,259 @@
+"""Benchmark of the compose hot path on one MI355X: reposition+splice of a
+precompiled skill's KV into a destination cache, then causal suffix attention
+over the spliced cache (paper Sec. 5: a re-rotation pass plus the suffix).
+
+One step = pkv_reposition_splice over every layer and KV head, then
+pkv_suffix_attention over every layer, on synthetic seeded inputs resident in
+HBM.  Default workload: Llama-3-8B-shaped single sequence (32 layers, 32/8
+heads, d 128, RoPE theta 5e5, 4096-token skill spliced at 2000 into 8192
+slots, 64-token suffix over 8256 slots, bf16).
+
+Prints one JSON line: the splice GB/s as `value`, the attention time and
+TFLOP/s beside it, the roofline of the dominant kernel (timed with HIP events
+on the library's stream), and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2606_17107_amd import pkv, synth  # noqa: E402
+
+METRIC = "KV reposition+splice GB/s; suffix prefix-attention µs and TFLOP/s"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+FP32_PEAK_TFLOPS = 157.3
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class GqaStep:
+    """Inputs and launches of one workload (single sequence, GQA or MLA)."""
+
+    def __init__(self, w: synth.Workload, n_splits: int, seed: int = 0):
+        self.w = w
+        dev = torch.device("cuda")
+        c = synth.gqa_case(w, seed=seed, device=dev)
+        self.cache_k = c["ctx_k"]
+        self.cache_v = c.get("ctx_v")
+        self.skill_k = c["skill_k_pre"]
+        self.skill_v = c.get("skill_v")
+        self.src_pos = c["src_pos"].to(dev)
+        self.dst_pos = c["dst_pos"].to(dev)
+        self.q_pos = c["q_pos"].to(dev)
+        n, nq = w.skill_tokens, w.n_q
+        # Post-RoPE skill keys: rotate the pre-RoPE draws from position 0 to their
+        # source positions, in place (dst_pos[t] == t keeps slot t).
+        zeros = torch.zeros(n, dtype=torch.int32, device=dev)
+        pkv.reposition_splice(self.skill_k, None, self.skill_k, None, zeros, self.src_pos, w.theta, w.rope_dim,
+                              w.rope_offset, w.rope_style)
+        # Suffix keys sit in cache slots ctx..kv_len-1 at positions equal to their slots.
+        suf = self.cache_k[:, :, w.ctx_slots:]
+        t_idx = torch.arange(nq, dtype=torch.int32, device=dev)
+        pkv.reposition_splice(suf, None, suf, None, torch.full((nq,), -w.ctx_slots, dtype=torch.int32,
+                              device=dev), t_idx, w.theta, w.rope_dim, w.rope_offset, w.rope_style)
+        # Post-RoPE queries [L][n_q][H][d], rotated in place per (query, head) row.
+        self.q = c["q_pre"]
+        qv = self.q.permute(0, 2, 1, 3)          # [L][H][n_q][d] view for the rotation
+        pkv.reposition_splice(qv, None, qv, None, torch.full((nq,), -w.ctx_slots, dtype=torch.int32,
+                              device=dev), t_idx, w.theta, w.rope_dim, w.rope_offset, w.rope_style)
+        self.out = torch.zeros(w.n_layers, nq, w.n_heads, w.v_dim, dtype=self.q.dtype, device=dev)
+        self.kv_len = torch.tensor([w.kv_len], dtype=torch.int32, device=dev)
+        self.v_view = self.cache_k[..., : w.v_dim] if w.mla else self.cache_v
+        self.splice_layout = pkv.make_layout(self.skill_k, self.skill_v, self.cache_k, self.cache_v,
+                                             w.rope_offset, w.rope_style)
+        variant = pkv.PKV_ATTN_MLA if w.mla else pkv.PKV_ATTN_GQA
+        self.desc = pkv.make_attn_desc(self.q, self.cache_k, self.v_view, self.out, w.kv_len, variant=variant,
+                                       n_splits=n_splits)
+        self.ws_bytes = pkv.pkv_attention_workspace_size(self.desc, w.n_heads, w.n_kv_heads, w.head_dim)
+        self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device=dev)
+        torch.cuda.synchronize()
+
+    def splice(self, stream):
+        w = self.w
+        st = pkv.pkv_reposition_splice(self.skill_k, self.skill_v, self.cache_k, self.cache_v, self.src_pos,
+                                       self.dst_pos, w.theta, w.rope_dim, self.splice_layout, stream)
+        if st != 0:
+            raise pkv.PkvError(st, pkv.pkv_last_error())
+
+    def attention(self, stream):
+        w = self.w
+        st = pkv.pkv_suffix_attention(self.q, self.cache_k, self.v_view, self.out, self.q_pos, self.kv_len,
+                                      w.n_heads, w.n_kv_heads, w.head_dim, w.scale, self.desc, self.ws,
+                                      self.ws_bytes, stream)
+        if st != 0:
+            raise pkv.PkvError(st, pkv.pkv_last_error())
+
+    def splice_bytes(self):
+        return self.w.splice_bytes()
+
+    def attn_flops(self):
+        return self.w.attn_flops()
+
+    def attn_bytes(self):
+        return self.w.attn_bytes()
+
+
+def cpu_baseline(w: synth.Workload, budget_s: float = 20.0):
+    """Time the fp64 oracle on a bounded sample of the same workload on the host cores."""
+    import numpy as np
+
+    import oracle
+
+    oracle.build(force=False)
+    threads = oracle.max_threads()
+    # splice sample: all tokens of the skill, a subset of layers
+    L_s = max(1, min(w.n_layers, 8))
+    c = synth.gqa_case(w, seed=1, layers=L_s)
+    bits = synth.to_numpy_bits
+    sk, dk = bits(c["skill_k_pre"]), bits(c["ctx_k"])
+    sv = bits(c["skill_v"]) if "skill_v" in c else None
+    dv = bits(c["ctx_v"]) if "ctx_v" in c else None
+    src, dst = c["src_pos"].numpy(), c["dst_pos"].numpy()
+    t0 = time.perf_counter()
+    oracle.reposition_splice(sk, sv, dk, dv, src, dst, w.theta, w.rope_dim, w.rope_offset, w.rope_style)
+    t_splice = time.perf_counter() - t0
+    sample_bytes = w.splice_bytes() * L_s / w.n_layers
+    # attention sample: one layer, a subset of queries, scaled by flops
+    q = bits(c["q_pre"][0])
+    k = dk[0]
+    v = dk[0][..., : w.v_dim] if w.mla else dv[0]
+    q_pos = c["q_pos"].numpy()
+    n_rows = w.n_q
+    est = w.attn_flops() / w.n_layers / 2e9 / max(threads, 1)   # ~2 GFLOP/s per core
+    if est > budget_s:
+        n_rows = max(1, int(w.n_q * budget_s / est))
+    t0 = time.perf_counter()
+    oracle.attention(np.ascontiguousarray(q[:n_rows]), k, v, q_pos[:n_rows], w.kv_len, w.scale)
+    t_attn = time.perf_counter() - t0
+    vis = sum(min(w.kv_len, int(q_pos[i]) + 1) for i in range(n_rows))
+    vis_all = sum(min(w.kv_len, int(q_pos[i]) + 1) for i in range(w.n_q))
+    attn_us_full = t_attn * (vis_all / vis) * w.n_layers * 1e6
+    return {
+        "value": round(sample_bytes / t_splice / 1e9, 4),
+        "unit": "GB/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": "splice: all %d skill tokens x %d of %d layers (%.3f GB in %.2f s); attention: layer 0, "
+                  "%d of %d queries (%.2f s), extrapolated to all layers and queries"
+                  % (w.skill_tokens, L_s, w.n_layers, sample_bytes / 1e9, t_splice, n_rows, w.n_q, t_attn),
+        "attention_us_extrapolated": round(attn_us_full, 1),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="gqa8b", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--splits", type=int, default=0, help="KV splits for attention (0 = library choice)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(reposition+splice and suffix attention run on a single MI355X)", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    pkv.lib()   # fail loudly if libpkv.so is missing
+
+    w = synth.WORKLOADS[args.workload]
+    log("workload", w)
+    step = GqaStep(w, args.splits)
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+
+    for _ in range(args.warmup):
+        step.splice(sh)
+        step.attention(sh)
+    torch.cuda.synchronize()
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record(stream)
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        step.splice(sh)
+        ev[i][1].record(stream)
+        step.attention(sh)
+        ev[i][2].record(stream)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    total_ms = start.elapsed_time(stop)
+    splice_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
+    attn_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
+    ms_per_step = total_ms / args.steps
+
+    splice_gbs = step.splice_bytes() / (splice_ms * 1e-3) / 1e9
+    attn_tflops = step.attn_flops() / (attn_ms * 1e-3) / 1e12
+    attn_gbs = step.attn_bytes() / (attn_ms * 1e-3) / 1e9
+    ai = step.attn_flops() / step.attn_bytes()
+    ridge = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+    attn_bound = "hbm" if ai < ridge else "mfma"
+    if attn_bound == "hbm":
+        attn_roof = {"bound": "hbm", "achieved": round(attn_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(attn_gbs / HBM_PEAK_GBS, 4), "traffic": None}
+    else:
+        attn_roof = {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4), "traffic": None}
+    splice_roof = {"bound": "hbm", "achieved": round(splice_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                   "frac": round(splice_gbs / HBM_PEAK_GBS, 4), "traffic": None}
+    splice_roof["kernel"] = "splice_kernel"
+    attn_roof["kernel"] = "attn_gqa_bf16" if not w.mla else "attn_mla_bf16"
+    dominant = splice_roof if splice_ms >= attn_ms else attn_roof
+
+    result = {
+        "metric": METRIC,
+        "value": round(splice_gbs, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s: %d layers, %d/%d heads, d %d, %d-token skill %d->%d, %d-token suffix over %d slots"
+                        % (w.name, w.n_layers, w.n_heads, w.n_kv_heads, w.head_dim, w.skill_tokens, w.src_pos0,
+                           w.dst_pos0, w.n_q, w.kv_len),
+            "splice_bytes": step.splice_bytes(),
+            "attention_flops": step.attn_flops(),
+            "attention_bytes": step.attn_bytes(),
+            "attention_splits": int(step.desc.n_splits) or "auto",
+            "workspace_bytes": step.ws_bytes,
+        },
+        "splice": {"us": round(splice_ms * 1e3, 2), "gbps": round(splice_gbs, 1)},
+        "attention": {"us": round(attn_ms * 1e3, 2), "tflops": round(attn_tflops, 2), "gbps": round(attn_gbs, 1),
+                      "arith_intensity": round(ai, 1), "bound": attn_bound},
+        "roofline": dominant,
+        "roofline_kernels": [splice_roof, attn_roof],
+        "wall_s_timed": round(t_wall, 3),
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

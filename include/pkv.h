@@ -1,0 +1,234 @@
+/*
+ * libpkv — MI355X (gfx950) kernels for moving a precompiled chunk of a
+ * post-RoPE KV cache to new positions and for the causal attention of the
+ * suffix that follows it.
+ *
+ * Source of the operations: "Models Take Notes at Prefill: KV Cache Can Be
+ * Editable and Composable".
+ *   - Sec. 5 ("From mechanism to prediction") and Fig. "Two cache operations"
+ *     (b): a chunk's KV is computed once at source positions; because the
+ *     cache stores post-RoPE keys, moving it re-rotates every key from its
+ *     source position to its target position, values are position-free, and
+ *     the result is spliced into the destination cache without a reprefill.
+ *     App. B's skill example fixes the source positions 0..L-1 and a target
+ *     offset.
+ *   - Sec. 8 (MLA adapter) and Fig. "attention-variant adapters" (a): an MLA
+ *     cache row holds a position-free latent plus a small decoupled-RoPE k_pe
+ *     slice; repositioning rotates only k_pe and copies the latent as-is.
+ *   - Sec. 5 ("Linear-time TTFT"): the transplant costs a re-rotation pass plus
+ *     the suffix; the suffix (or an appended erratum, Sec. 4) attends causally
+ *     over the spliced cache.
+ *
+ * Conventions for every call:
+ *   - All tensor and index pointers are DEVICE pointers owned by the caller.
+ *     The library never allocates, frees or retains them.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Calls enqueue
+ *     work and return; kernel faults surface at the caller's next
+ *     synchronisation.  No call synchronises the device.
+ *   - Strides are in ELEMENTS.  The channel dimension of every row is
+ *     contiguous.
+ *   - On a non-OK status nothing was enqueued, and pkv_last_error() returns a
+ *     message for the calling thread.
+ *   - bf16 is stored as its 16-bit pattern; fp32 as IEEE binary32.
+ *
+ * RoPE convention (the paper names RoPE but does not write its pairing or
+ * frequencies out): pair i of the rotary slice [rope_offset, rope_offset +
+ * rope_dim) has frequency omega_i = rope_theta^(-2i/rope_dim), and rotating
+ * by an integer position multiple p maps (a, b) to
+ * (a cos(p omega_i) - b sin(p omega_i), a sin(p omega_i) + b cos(p omega_i)).
+ * PKV_ROPE_HALF pairs channel o+i with o+i+rope_dim/2; PKV_ROPE_INTERLEAVED
+ * pairs o+2i with o+2i+1.
+ */
+#ifndef PKV_H
+#define PKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PKV_VERSION 1
+
+typedef enum pkv_status {
+    PKV_OK = 0,
+    PKV_ERR_NULL = 1,         /* a required pointer is NULL */
+    PKV_ERR_SHAPE = 2,        /* inconsistent sizes, rope slice outside the row, workspace too small */
+    PKV_ERR_ALIGN = 3,        /* a pointer or stride is not 16-byte aligned */
+    PKV_ERR_ALIAS = 4,        /* source and destination memory partially overlap */
+    PKV_ERR_UNSUPPORTED = 5,  /* dtype / head size / rope geometry this build does not implement */
+    PKV_ERR_DEVICE = 6        /* the HIP runtime refused the launch (message has its text) */
+} pkv_status;
+
+enum { PKV_BF16 = 0, PKV_F32 = 1 };
+enum { PKV_ROPE_HALF = 0, PKV_ROPE_INTERLEAVED = 1 };
+enum { PKV_ATTN_GQA = 0, PKV_ATTN_MLA = 1 };
+
+/* ---------------------------------------------------------------------------
+ * Reposition + splice
+ * ------------------------------------------------------------------------- */
+
+/* Geometry of one splice.  K tensors are indexed [layer][kv_head][slot][channel]
+ * through the strides below (any order of the three outer dimensions works;
+ * e.g. token-major [layer][slot][kv_head][d] caches pass the matching
+ * strides).  V tensors likewise with v_dim channels.
+ *
+ * Geometry this build implements (else PKV_ERR_UNSUPPORTED), with
+ * E = 16 / element size (8 for bf16, 4 for fp32):
+ *   head_dim, v_dim, rope_offset multiples of E; head_dim and v_dim multiples
+ *   of 2E; rope_dim a multiple of 2E.  This covers d = 64/128 GQA heads and
+ *   the 576-channel MLA row [c_kv (512) | k_pe (64)] with rope_offset 512. */
+typedef struct pkv_layout {
+    int32_t dtype;          /* PKV_BF16 or PKV_F32 */
+    int32_t n_layers;
+    int32_t n_kv_heads;     /* 1 for an MLA latent row */
+    int32_t head_dim;       /* channels of a K row (576 for MLA) */
+    int32_t v_dim;          /* channels of a V row; 0 = no V tensors (MLA: src_v, dst_v must be NULL) */
+    int32_t n_tokens;       /* pkv_reposition_splice: tokens to move (source slots 0..n_tokens-1).
+                               pkv_reposition_splice_batched: number of source slots in src_k/src_v */
+    int32_t rope_offset;    /* first rotary channel of a K row */
+    int32_t rope_style;     /* PKV_ROPE_HALF or PKV_ROPE_INTERLEAVED */
+    int32_t dst_capacity;   /* destination slots 0..dst_capacity-1 exist in dst_k/dst_v */
+    int32_t reserved;       /* must be 0 */
+    int64_t src_k_stride[3];   /* {layer, head, slot} */
+    int64_t src_v_stride[3];
+    int64_t dst_k_stride[3];
+    int64_t dst_v_stride[3];
+    int32_t* err_flag;      /* optional device int32: set to 1 when a token is skipped because its
+                               destination (or, batched, its source) slot is out of range */
+} pkv_layout;
+
+/* Reposition + splice of one chunk (Sec. 5; Fig. "Two cache operations" (b);
+ * Sec. 8 MLA adapter).  For every layer l, KV head h and token t < n_tokens,
+ * with delta_t = dst_pos[t] - src_pos[t]:
+ *     dst_k[l][h][dst_pos[t]] = R(delta_t) src_k[l][h][t]   (rotary slice; other channels bit-exact)
+ *     dst_v[l][h][dst_pos[t]] = src_v[l][h][t]              (bit-exact)
+ * src_pos / dst_pos: device int32 [n_tokens], any sign, |delta| < 2^24.
+ * Rotation arithmetic: the angle delta*omega_i and its cos/sin are formed in
+ * fp64, rounded to fp32, and the rotation runs in fp32 with one
+ * round-to-nearest-even to the storage type.  delta_t == 0 copies the row
+ * bit-exact.  Destination slots other than dst_pos[] are not touched.  A token
+ * with dst_pos outside [0, dst_capacity) is skipped (and *err_flag set).
+ * In-place use (dst_k == src_k with identical strides, same for V) is allowed
+ * when dst_pos[t] == t for every t; any other overlap between a source and a
+ * destination tensor, or between dst_k and dst_v, is PKV_ERR_ALIAS.
+ * Errors: PKV_ERR_NULL (layout, src_k, dst_k, src_pos, dst_pos; src_v/dst_v
+ * when v_dim > 0), PKV_ERR_SHAPE (non-positive sizes, rope_dim odd or <= 0,
+ * rope slice outside the row, n_tokens < 0, theta <= 0), PKV_ERR_ALIGN,
+ * PKV_ERR_ALIAS, PKV_ERR_UNSUPPORTED, PKV_ERR_DEVICE. */
+pkv_status pkv_reposition_splice(const void* src_k, const void* src_v, void* dst_k, void* dst_v,
+                                 const int32_t* src_pos, const int32_t* dst_pos, float rope_theta,
+                                 int32_t rope_dim, const pkv_layout* layout, void* stream);
+
+/* One chunk of a multi-chunk composition (Sec. 5: a library of skills
+ * composes; Sec. 7 E4: memory split into independently precompiled blocks).
+ * Source tokens src_slot0 .. src_slot0+n_tokens-1 were encoded at positions
+ * src_pos0 .. ; they move to positions dst_pos0 .. of the destination
+ * sequence whose position 0 is slot dst_seq_base.  delta = dst_pos0 - src_pos0. */
+typedef struct pkv_segment {
+    int64_t src_slot0;
+    int64_t dst_seq_base;
+    int32_t n_tokens;
+    int32_t src_pos0;
+    int32_t dst_pos0;
+    int32_t dst_seq_len;    /* positions 0..dst_seq_len-1 exist in this sequence */
+} pkv_segment;
+
+/* Reposition + splice of many chunks into many sequences in one launch.
+ * segs: DEVICE array of n_segs segments.  max_seg_tokens must be >= every
+ * segs[i].n_tokens (host-known bound used to size the grid).  layout->n_tokens
+ * is the number of source slots in src_k/src_v and layout->dst_capacity the
+ * number of destination slots; a token whose source slot, destination
+ * position or destination slot falls outside those ranges is skipped (and
+ * *err_flag set).  Segments must not write overlapping destination slots.
+ * Same arithmetic, copy and aliasing rules as pkv_reposition_splice (no
+ * in-place use).  Errors: as pkv_reposition_splice, plus PKV_ERR_SHAPE when
+ * n_segs < 0 or max_seg_tokens < 0. */
+pkv_status pkv_reposition_splice_batched(const void* src_k, const void* src_v, void* dst_k,
+                                         void* dst_v, const pkv_segment* segs, int32_t n_segs,
+                                         int32_t max_seg_tokens, float rope_theta, int32_t rope_dim,
+                                         const pkv_layout* layout, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Suffix attention
+ * ------------------------------------------------------------------------- */
+
+/* Geometry of a suffix-attention call over n_layers layers and n_seqs
+ * sequences.  Query rows of all sequences are packed: sequence s owns rows
+ * cu_q[s] .. cu_q[s+1]-1 of q/out/q_pos.  Its cache occupies slots
+ * kv_base[s] .. kv_base[s]+kv_len[s]-1 of k_cache/v_cache.
+ *   q    [layer][row][q_head][head_dim]      strides q_stride   {layer, row, head}
+ *   out  [layer][row][q_head][head_dim_v]    strides o_stride   {layer, row, head}
+ *   k    [layer][kv_head][slot][head_dim]    strides k_stride   {layer, head, slot}
+ *   v    [layer][kv_head][slot][head_dim_v]  strides v_stride   {layer, head, slot}
+ * MLA (variant PKV_ATTN_MLA, absorbed form): n_kv_heads = 1, head_dim = 576
+ * (512 latent + 64 k_pe), head_dim_v = 512, and v_cache may equal k_cache (the
+ * latent is the first 512 channels of each row). */
+typedef struct pkv_attn_desc {
+    int32_t dtype;          /* PKV_BF16 (MFMA path) or PKV_F32 (GQA only) */
+    int32_t variant;        /* PKV_ATTN_GQA or PKV_ATTN_MLA */
+    int32_t n_layers;
+    int32_t n_seqs;
+    int32_t head_dim_v;     /* == head_dim for GQA; 512 for MLA */
+    int32_t total_q;        /* query rows per layer over all sequences */
+    int32_t max_q;          /* >= the largest per-sequence query count */
+    int32_t max_kv_len;     /* >= every kv_len[s]; larger values are clamped to it */
+    int32_t n_splits;       /* KV-length splits; 0 = the library chooses */
+    int32_t reserved;       /* must be 0 */
+    const int32_t* cu_q;    /* device int32 [n_seqs+1]; NULL allowed when n_seqs == 1 */
+    const int64_t* kv_base; /* device int64 [n_seqs]; NULL = every sequence starts at slot 0 */
+    int64_t cache_slots;    /* slots present in k_cache/v_cache; reads past it are masked out */
+    int64_t q_stride[3];
+    int64_t k_stride[3];
+    int64_t v_stride[3];
+    int64_t o_stride[3];
+    float* lse_out;         /* optional device fp32 [n_layers][total_q][n_q_heads]: natural-log
+                               log-sum-exp of the visible scaled scores (-inf for an empty row) */
+} pkv_attn_desc;
+
+/* Bytes of device workspace pkv_suffix_attention needs for `desc` (split-KV
+ * partial outputs and their log-sum-exps, fp32).  0 when no split is used.
+ * Returns 0 on invalid arguments as well (pkv_suffix_attention reports them). */
+size_t pkv_attention_workspace_size(const pkv_attn_desc* desc, int32_t n_q_heads, int32_t n_kv_heads,
+                                    int32_t head_dim);
+
+/* Causal attention of the suffix/erratum queries over the spliced cache
+ * (Sec. 5 "Linear-time TTFT"; Sec. 4 erratum; Sec. 6 delta prefill).  For layer
+ * l, query row i of sequence s and query head h (KV head g = h / (n_q_heads /
+ * n_kv_heads)):
+ *     visible j: 0 <= j < kv_len[s], j <= q_pos[i]
+ *     out[l][i][h] = sum_j softmax_j(scale * <q[l][i][h], k[l][g][kv_base[s]+j]>) v[l][g][kv_base[s]+j]
+ * q is post-RoPE (q_pos only masks).  bf16: QK^T and PV on bf16 MFMA with fp32
+ * accumulation, softmax statistics in fp32, probabilities rounded to bf16
+ * before PV, output rounded to bf16.  fp32: fp32 FMA throughout.  A row with no
+ * visible slot is written as zeros.  q_pos: device int32 [total_q]; kv_len:
+ * device int32 [n_seqs].  workspace: device memory of at least
+ * pkv_attention_workspace_size() bytes (may be NULL when that is 0), owned by
+ * the caller, contents scratch.
+ * Errors: PKV_ERR_NULL, PKV_ERR_SHAPE (n_q_heads % n_kv_heads != 0, sizes <= 0,
+ * workspace too small, MLA shape not 576/512 with one KV head), PKV_ERR_ALIGN,
+ * PKV_ERR_UNSUPPORTED (head_dim other than 64 or 128 for GQA; fp32 MLA),
+ * PKV_ERR_DEVICE. */
+pkv_status pkv_suffix_attention(const void* q, const void* k_cache, const void* v_cache, void* out,
+                                const int32_t* q_pos, const int32_t* kv_len, int32_t n_q_heads,
+                                int32_t n_kv_heads, int32_t head_dim, float scale,
+                                const pkv_attn_desc* desc, void* workspace, size_t workspace_bytes,
+                                void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Diagnostics
+ * ------------------------------------------------------------------------- */
+
+/* Message for the last non-OK status returned on the calling thread ("" if
+ * none).  The pointer stays valid until the next libpkv call on this thread. */
+const char* pkv_last_error(void);
+
+/* PKV_VERSION of the built library. */
+int32_t pkv_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PKV_H */

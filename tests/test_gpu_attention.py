@@ -1,0 +1,242 @@
+"""GPU parity of pkv_suffix_attention against the fp64 oracle (paper Sec. 5
+"Linear-time TTFT": the suffix attends causally over the spliced cache;
+Sec. 4 erratum; Sec. 6 delta prefill).
+
+Bar for bf16 outputs (fp32 accumulation): max-abs <= 2e-2, mean-abs <= 2e-3,
+and relative L2 <= 1e-2; N(0,1) queries give a flat softmax, so sharpened
+(Q x 4) and planted-needle cases are added.  fp32 path: relative L2 <= 1e-5."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from helpers import bits_to_f64, check_attention_close, dev, host_bits, log, rope_cache, rope_queries, small_workload
+from paper_2606_17107_amd import pkv, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def assemble_cache(w, c):
+    """Host cache for workload w: context draws, the skill spliced by the oracle, suffix K/V appended
+    (suffix keys RoPE'd at their positions), and the post-RoPE queries."""
+    ctx_k = host_bits(c["ctx_k"])
+    ctx_v = host_bits(c["ctx_v"]) if "ctx_v" in c else None
+    src, dst, q_pos = c["src_pos"].numpy(), c["dst_pos"].numpy(), c["q_pos"].numpy()
+    skill_k = rope_cache(host_bits(c["skill_k_pre"]), src[None, None, :], w)
+    skill_v = host_bits(c["skill_v"]) if "skill_v" in c else None
+    oracle.reposition_splice(skill_k, skill_v, ctx_k, ctx_v, src, dst, w.theta, w.rope_dim, w.rope_offset,
+                             w.rope_style)
+    ctx_k[:, :, q_pos] = rope_cache(host_bits(c["suf_k_pre"]), q_pos[None, None, :], w)
+    if ctx_v is not None:
+        ctx_v[:, :, q_pos] = host_bits(c["suf_v"])
+    q = rope_queries(host_bits(c["q_pre"]), q_pos, w)
+    return q, ctx_k, ctx_v, q_pos
+
+
+def gpu_attention(w, q, k, v, q_pos, kv_len, n_splits=0, lse=False, variant=pkv.PKV_ATTN_GQA):
+    qd, kd = dev(q), dev(k)
+    vd = kd[..., : w.v_dim] if v is None else dev(v)
+    L, nq, H = q.shape[:3]
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    out = torch.zeros(L, nq, H, w.v_dim, dtype=dt, device="cuda")
+    lse_t = torch.zeros(L, nq, H, dtype=torch.float32, device="cuda") if lse else None
+    qp = torch.from_numpy(q_pos.astype(np.int32)).cuda()
+    kl = torch.tensor([kv_len], dtype=torch.int32, device="cuda")
+    pkv.suffix_attention(qd, kd, vd, out, qp, kl, w.scale, max_kv_len=kv_len, variant=variant,
+                         n_splits=n_splits, lse_out=lse_t)
+    torch.cuda.synchronize()
+    o = host_bits(out)
+    return (o, lse_t.cpu().numpy()) if lse else o
+
+
+def oracle_attention(w, q, k, v, q_pos, kv_len, layers=None, rows=None):
+    outs, lses = [], []
+    for l in (range(q.shape[0]) if layers is None else layers):
+        qq = q[l] if rows is None else np.ascontiguousarray(q[l][rows])
+        qp = q_pos if rows is None else q_pos[rows]
+        vv = k[l][..., : w.v_dim] if v is None else v[l]
+        o, s = oracle.attention(qq, k[l], vv, qp, kv_len, w.scale)
+        outs.append(o)
+        lses.append(s)
+    return np.stack(outs), np.stack(lses)
+
+
+def test_tiny_fp32_config():
+    w = synth.TINY
+    c = synth.gqa_case(w, seed=0)
+    q, k, v, q_pos = assemble_cache(w, c)
+    log("tiny fp32 attention")
+    got, lse = gpu_attention(w, q, k, v, q_pos, w.kv_len, lse=True)
+    want, want_lse = oracle_attention(w, q, k, v, q_pos, w.kv_len)
+    rl2 = np.linalg.norm(got - want) / np.linalg.norm(want)
+    assert rl2 <= 1e-5, rl2
+    assert np.abs(got - want).max() <= 1e-5
+    np.testing.assert_allclose(lse, want_lse, rtol=1e-5, atol=1e-5)
+
+
+SMALL = [
+    dict(H=8, Hkv=2, d=128, n_q=45, ctx=400, splits=1),
+    dict(H=8, Hkv=2, d=128, n_q=45, ctx=400, splits=3),
+    dict(H=8, Hkv=2, d=64, n_q=33, ctx=700, splits=0),
+    dict(H=14, Hkv=2, d=128, n_q=19, ctx=257, splits=2),     # G = 7: rows straddle queries
+    dict(H=4, Hkv=4, d=128, n_q=70, ctx=130, splits=1),      # G = 1 (MHA)
+    dict(H=32, Hkv=8, d=128, n_q=64, ctx=1000, splits=0),
+]
+
+
+@pytest.mark.parametrize("cfg", SMALL, ids=lambda c: "H%d_Hkv%d_d%d_q%d_c%d_s%d" % tuple(c.values()))
+def test_small_bf16(cfg):
+    w = small_workload(L=2, H=cfg["H"], Hkv=cfg["Hkv"], d=cfg["d"], theta=1e4, skill=min(150, cfg["ctx"] - 40),
+                       dst0=20, ctx=cfg["ctx"], n_q=cfg["n_q"])
+    c = synth.gqa_case(w, seed=1)
+    q, k, v, q_pos = assemble_cache(w, c)
+    log("small bf16 attention", cfg)
+    got, lse = gpu_attention(w, q, k, v, q_pos, w.kv_len, n_splits=cfg["splits"], lse=True)
+    want, want_lse = oracle_attention(w, q, k, v, q_pos, w.kv_len)
+    log("  ", check_attention_close(got, want))
+    np.testing.assert_allclose(lse, want_lse, atol=2e-2)
+
+
+def test_sharpened_queries():
+    """Q x 4 (exact in bf16) sharpens the softmax so the tolerance is far from vacuous."""
+    w = small_workload(L=2, H=8, Hkv=2, d=128, theta=1e4, skill=300, dst0=100, ctx=900, n_q=40)
+    c = synth.gqa_case(w, seed=2)
+    q, k, v, q_pos = assemble_cache(w, c)
+    q4 = synth.to_numpy_bits(synth.from_numpy_bits(q).float().mul(4).to(torch.bfloat16))
+    for splits in (1, 4):
+        got = gpu_attention(w, q4, k, v, q_pos, w.kv_len, n_splits=splits)
+        want, _ = oracle_attention(w, q4, k, v, q_pos, w.kv_len)
+        stats = check_attention_close(got, want, max_abs=2e-2, mean_abs=2e-3, rel_l2=1e-2)
+        log("  sharpened splits=%d" % splits, stats, "rms", float(np.sqrt((want ** 2).mean())))
+
+
+def test_planted_needle():
+    """A key aligned with one query row and large: that row's output is the needle's value row."""
+    w = small_workload(L=1, H=4, Hkv=1, d=128, theta=1e4, skill=100, dst0=10, ctx=600, n_q=8)
+    c = synth.gqa_case(w, seed=3)
+    q, k, v, q_pos = assemble_cache(w, c)
+    qf = bits_to_f64(q[0, 5, 2])                    # query 5, head 2
+    # score = scale * 4 |q|^2 ~ 45 for d 128: exp(45) dominates the ~600 N(0,1)-scored slots
+    needle = synth.to_numpy_bits(torch.from_numpy((qf * 4.0).astype(np.float32)).to(torch.bfloat16))
+    k[0, 0, 333] = needle
+    for splits in (1, 5):
+        got = gpu_attention(w, q, k, v, q_pos, w.kv_len, n_splits=splits)
+        want, _ = oracle_attention(w, q, k, v, q_pos, w.kv_len)
+        check_attention_close(got, want)
+        np.testing.assert_allclose(bits_to_f64(got[0, 5, 2]), bits_to_f64(v[0, 0, 333]), atol=3e-2)
+
+
+def test_irregular_positions_and_empty_rows():
+    """q_pos need not be contiguous; a row that sees no slot (q_pos < 0) is zero."""
+    w = small_workload(L=2, H=8, Hkv=2, d=128, theta=1e4, skill=100, dst0=10, ctx=500, n_q=24)
+    c = synth.gqa_case(w, seed=4)
+    q, k, v, _ = assemble_cache(w, c)
+    q_pos = np.array([-1, 0, 1, 63, 64, 65, 127, 128, 200, 511, 523, 3, 77, 300, 301, 302, 450, 460, 470, 480,
+                      490, 500, 510, 520], np.int32)
+    for splits in (1, 3):
+        got, lse = gpu_attention(w, q, k, v, q_pos, w.kv_len, n_splits=splits, lse=True)
+        want, want_lse = oracle_attention(w, q, k, v, q_pos, w.kv_len)
+        assert np.all(got[:, 0] == 0) and np.all(np.isneginf(lse[:, 0]))
+        check_attention_close(got[:, 1:], want[:, 1:])
+        np.testing.assert_allclose(bits_to_f64(got[:, 1]), bits_to_f64(v[:, np.repeat(np.arange(2), 4), 0]),
+                                   atol=1e-6)
+
+
+def test_ragged_sequences():
+    """Several sequences packed in one call: per-sequence query ranges, cache bases and lengths."""
+    H, Hkv, d = 8, 2, 128
+    nqs = [17, 40, 1, 64]
+    kvls = [300, 1000, 77, 513]
+    L = 2
+    g = synth.Draws(5, "cpu")
+    caps = [kl + 11 for kl in kvls]
+    bases = np.concatenate([[0], np.cumsum(caps)[:-1]]).astype(np.int64)
+    total_slots = int(sum(caps))
+    k = host_bits(g.normal((L, Hkv, total_slots, d)))
+    v = host_bits(g.normal((L, Hkv, total_slots, d)))
+    q = host_bits(g.normal((L, sum(nqs), H, d)))
+    q_pos = np.concatenate([np.arange(kl - n, kl) for n, kl in zip(nqs, kvls)]).astype(np.int32)
+    cu = np.concatenate([[0], np.cumsum(nqs)]).astype(np.int32)
+    w = small_workload(L=L, H=H, Hkv=Hkv, d=d)
+    for splits in (1, 4):
+        out = torch.zeros(L, sum(nqs), H, d, dtype=torch.bfloat16, device="cuda")
+        pkv.suffix_attention(dev(q), dev(k), dev(v), out, torch.from_numpy(q_pos).cuda(),
+                             torch.tensor(kvls, dtype=torch.int32, device="cuda"), w.scale, max_kv_len=max(kvls),
+                             n_seqs=len(nqs), cu_q=torch.from_numpy(cu).cuda(),
+                             kv_base=torch.from_numpy(bases).cuda(), max_q=max(nqs), n_splits=splits)
+        torch.cuda.synchronize()
+        got = host_bits(out)
+        for s in range(len(nqs)):
+            rows = slice(cu[s], cu[s + 1])
+            ks = slice(bases[s], bases[s] + caps[s])
+            for l in range(L):
+                want, _ = oracle.attention(np.ascontiguousarray(q[l, rows]), np.ascontiguousarray(k[l][:, ks]),
+                                           np.ascontiguousarray(v[l][:, ks]), q_pos[rows], kvls[s], w.scale)
+                check_attention_close(got[l, rows], want)
+
+
+def test_transplant_then_attend_matches_recompute():
+    """End to end on the GPU: splice(RoPE(k, src)) then attention equals the oracle's attention over a
+    cache holding RoPE(k, dst) directly."""
+    w = small_workload(L=2, H=8, Hkv=2, d=128, theta=5e5, skill=300, dst0=200, ctx=800, n_q=32)
+    c = synth.gqa_case(w, seed=6)
+    src, dst, q_pos = c["src_pos"].numpy(), c["dst_pos"].numpy(), c["q_pos"].numpy()
+    k_pre = host_bits(c["skill_k_pre"])
+    ctx_k, ctx_v = host_bits(c["ctx_k"]), host_bits(c["ctx_v"])
+    ctx_k[:, :, q_pos] = rope_cache(host_bits(c["suf_k_pre"]), q_pos[None, None, :], w)
+    ctx_v[:, :, q_pos] = host_bits(c["suf_v"])
+    q = rope_queries(host_bits(c["q_pre"]), q_pos, w)
+    # GPU: RoPE the skill at its source positions in place, splice, attend
+    sk = dev(k_pre)
+    pkv.reposition_splice(sk, None, sk, None, torch.zeros_like(c["src_pos"]).cuda(), c["src_pos"].cuda(),
+                          w.theta, w.rope_dim)
+    kd, vd = dev(ctx_k), dev(ctx_v)
+    pkv.reposition_splice(sk, dev(host_bits(c["skill_v"])), kd, vd, c["src_pos"].cuda(), c["dst_pos"].cuda(),
+                          w.theta, w.rope_dim)
+    out = torch.zeros(2, w.n_q, w.n_heads, w.head_dim, dtype=torch.bfloat16, device="cuda")
+    pkv.suffix_attention(dev(q), kd, vd, out, c["q_pos"].cuda(), torch.tensor([w.kv_len], dtype=torch.int32,
+                         device="cuda"), w.scale, max_kv_len=w.kv_len)
+    torch.cuda.synchronize()
+    # oracle: the skill placed directly at its destination positions
+    direct_k, direct_v = ctx_k.copy(), ctx_v.copy()
+    direct_k[:, :, dst] = rope_cache(k_pre, dst[None, None, :], w)
+    direct_v[:, :, dst] = host_bits(c["skill_v"])
+    want, _ = oracle_attention(w, q, direct_k, direct_v, q_pos, w.kv_len)
+    log("  transplant vs recompute", check_attention_close(host_bits(out), want))
+
+
+def test_determinism():
+    w = small_workload(L=2, H=8, Hkv=2, d=128, skill=100, dst0=10, ctx=2000, n_q=64)
+    c = synth.gqa_case(w, seed=7)
+    q, k, v = host_bits(c["q_pre"]), host_bits(c["ctx_k"]), host_bits(c["ctx_v"])
+    q_pos = c["q_pos"].numpy()
+    a = gpu_attention(w, q, k, v, q_pos, w.kv_len, n_splits=4)
+    b = gpu_attention(w, q, k, v, q_pos, w.kv_len, n_splits=4)
+    np.testing.assert_array_equal(a, b)
+
+
+# ---- full-size workloads, sampled against the oracle ---------------------------
+
+def full_gqa(w, layers, rows, seed=0):
+    c = synth.gqa_case(w, seed=seed, device="cuda")
+    q, k, v = c["q_pre"], c["ctx_k"], c["ctx_v"]
+    out = torch.zeros(w.n_layers, w.n_q, w.n_heads, w.head_dim, dtype=torch.bfloat16, device="cuda")
+    log("full-size attention", w.name, "layers", layers, "rows", len(rows))
+    pkv.suffix_attention(q, k, v, out, c["q_pos"].cuda(), torch.tensor([w.kv_len], dtype=torch.int32,
+                         device="cuda"), w.scale, max_kv_len=w.kv_len)
+    torch.cuda.synchronize()
+    got = host_bits(out[layers][:, rows])
+    qh, kh, vh = host_bits(q[layers]), host_bits(k[layers]), host_bits(v[layers])
+    want, _ = oracle_attention(w, qh, kh, vh, c["q_pos"].numpy(), w.kv_len, rows=rows)
+    log("  ", check_attention_close(got, want))
+
+
+def test_full_gqa8b():
+    full_gqa(synth.GQA8B, layers=[0, 31], rows=np.arange(64))
+
+
+def test_full_long32k_sampled():
+    rows = np.unique(np.concatenate([[0, 1, 511, 1022, 1023], np.random.default_rng(0).integers(0, 1024, 11)]))
+    full_gqa(synth.LONG32K, layers=[0, 27], rows=rows)
