@@ -1,0 +1,111 @@
+// Device-side pieces shared by the suffix-attention kernels: the work plan,
+// the XCD-aware workgroup decode, per-sequence bounds and small wave helpers.
+#pragma once
+
+#include <math.h>
+
+#include "pkv_internal.h"
+
+namespace pkv {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+#ifndef PKV_LDS
+#define PKV_LDS(T, p) ((__attribute__((address_space(3))) T*)(p))
+#endif
+
+constexpr int kXcds = 8;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+struct Plan {
+    int G;          // query heads per KV head
+    int BM;         // rows per workgroup
+    int rbs;        // row blocks per group
+    int n_groups;   // layers x kv heads x sequences x splits
+    int splits;
+    int chunk;      // keys per split (multiple of the key tile)
+    int qb, nw, ns; // bf16 GQA kernel shape: 32-row blocks per wave, waves, LDS stages
+};
+
+// Workgroup id -> (group, row block).  Workgroups are dispatched round-robin
+// over the 8 XCDs by id; giving every row block of a group (which all read the
+// same K/V range) an id with the same residue mod 8 keeps them on one XCD, at
+// consecutive dispatch slots, so they share that XCD's L2.
+__device__ inline bool decode(const Plan& p, int& group, int& rb) {
+    const int id = blockIdx.x;
+    const int xcd = id % kXcds;
+    const int slot = id / kXcds;
+    rb = slot % p.rbs;
+    group = (slot / p.rbs) * kXcds + xcd;
+    return group < p.n_groups;
+}
+
+struct SeqInfo {
+    int q0, nq, kvl;
+    int64_t base;
+};
+
+__device__ inline SeqInfo seq_info(const AttnArgs& a, int seq) {
+    SeqInfo s;
+    if (a.cu_q) {
+        s.q0 = a.cu_q[seq];
+        s.nq = a.cu_q[seq + 1] - s.q0;
+    } else {
+        s.q0 = 0;
+        s.nq = a.total_q;
+    }
+    // Keep every row and slot index inside the tensors the caller described.
+    if (s.q0 < 0 || s.nq < 0 || (int64_t)s.q0 + s.nq > a.total_q) s.nq = 0;
+    s.base = a.kv_base ? a.kv_base[seq] : 0;
+    int64_t kvl = a.kv_len[seq];
+    if (s.base < 0) kvl = 0;
+    if (kvl > a.max_kv_len) kvl = a.max_kv_len;
+    if (kvl > a.cache_slots - s.base) kvl = a.cache_slots - s.base;
+    if (kvl < 0) kvl = 0;
+    s.kvl = (int)kvl;
+    return s;
+}
+
+__device__ inline int wave_max_i(int v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v = max(v, __shfl_xor(v, o));
+    return v;
+}
+__device__ inline int wave_min_i(int v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v = min(v, __shfl_xor(v, o));
+    return v;
+}
+
+__device__ inline uint32_t bf_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+// Wait until at most N vector-memory operations of this wave are outstanding
+// (gfx9 s_waitcnt encoding: vmcnt split over bits 3:0 and 15:14; expcnt and
+// lgkmcnt left at their "no wait" maxima).
+template <int N>
+__device__ inline void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier without the release/acquire fences of __syncthreads():
+// the fences would force the wave to drain every in-flight LDS-DMA load,
+// which is exactly what the staged pipeline must not do.  Ordering of the
+// LDS traffic around it is established by explicit s_waitcnt.
+__device__ inline void bare_barrier() {
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+}  // namespace pkv

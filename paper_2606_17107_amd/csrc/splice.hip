@@ -34,8 +34,36 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kUnroll = 4;
+// Launch-shape constants (tuned on MI355X; overridable at build time).
+#ifndef PKV_SPLICE_UNROLL
+#define PKV_SPLICE_UNROLL 4        // rows whose loads are issued before any is used
+#endif
+#ifndef PKV_SPLICE_TARGET_BLOCKS
+#define PKV_SPLICE_TARGET_BLOCKS 8192
+#endif
+#ifndef PKV_SPLICE_MIN_ROWS
+#define PKV_SPLICE_MIN_ROWS 8      // rows per thread at least (amortises the cos/sin)
+#endif
+#ifndef PKV_SPLICE_NONTEMPORAL
+#define PKV_SPLICE_NONTEMPORAL 1   // streaming loads/stores: the data is touched once
+#endif
+constexpr int kUnroll = PKV_SPLICE_UNROLL;
 constexpr int kHalf = 0;
+
+__device__ inline u32x4 ld16(const char* p) {
+#if PKV_SPLICE_NONTEMPORAL
+    return __builtin_nontemporal_load((const u32x4*)p);
+#else
+    return *(const u32x4*)p;
+#endif
+}
+__device__ inline void st16(char* p, u32x4 v) {
+#if PKV_SPLICE_NONTEMPORAL
+    __builtin_nontemporal_store(v, (u32x4*)p);
+#else
+    *(u32x4*)p = v;
+#endif
+}
 
 struct Geo {
     int lanes_k, lanes_v, lanes, tok_per_block, rows_per_block;
@@ -205,16 +233,16 @@ __global__ __launch_bounds__(256) void splice_kernel(SpliceArgs a, Geo g) {
                 const int head = rr - layer * a.n_kv_heads;
                 const int64_t so = ((int64_t)layer * s0 + (int64_t)head * s1) * EB;
                 doff[u] = ((int64_t)layer * d0 + (int64_t)head * d1) * EB;
-                va[u] = __builtin_nontemporal_load((const u32x4*)(sbase + so + oa));
-                vb[u] = __builtin_nontemporal_load((const u32x4*)(sbase + so + ob));
+                va[u] = ld16(sbase + so + oa);
+                vb[u] = ld16(sbase + so + ob);
             }
         }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             if (r + u < r1) {
                 if (rope) rotate_chunks<EB, STYLE>(va[u], vb[u], cs, sn);
-                __builtin_nontemporal_store(va[u], (u32x4*)(dbase + doff[u] + oa));
-                __builtin_nontemporal_store(vb[u], (u32x4*)(dbase + doff[u] + ob));
+                st16(dbase + doff[u] + oa, va[u]);
+                st16(dbase + doff[u] + ob, vb[u]);
             }
         }
     }
@@ -256,10 +284,10 @@ hipError_t launch_splice(const SpliceArgs& a, hipStream_t stream) {
     const int64_t gx = (tokens + g.tok_per_block - 1) / g.tok_per_block;
     // Enough blocks to fill 256 CUs several times over, while every thread
     // still visits several rows so its cos/sin are reused.
-    int64_t want_y = (4096 + gx * nz - 1) / (gx * nz);
+    int64_t want_y = (PKV_SPLICE_TARGET_BLOCKS + gx * nz - 1) / (gx * nz);
     if (want_y < 1) want_y = 1;
     int rows = (int)((g.n_rows + want_y - 1) / want_y);
-    rows = rows < 8 ? (g.n_rows < 8 ? g.n_rows : 8) : rows;
+    rows = rows < PKV_SPLICE_MIN_ROWS ? (g.n_rows < PKV_SPLICE_MIN_ROWS ? g.n_rows : PKV_SPLICE_MIN_ROWS) : rows;
     g.rows_per_block = rows;
     const int gy = (g.n_rows + rows - 1) / rows;
 
