@@ -163,8 +163,9 @@ pkv_status pkv_reposition_splice_batched(const void* src_k, const void* src_v, v
  *   k    [layer][kv_head][slot][head_dim]    strides k_stride   {layer, head, slot}
  *   v    [layer][kv_head][slot][head_dim_v]  strides v_stride   {layer, head, slot}
  * MLA (variant PKV_ATTN_MLA, absorbed form): n_kv_heads = 1, head_dim = 576
- * (512 latent + 64 k_pe), head_dim_v = 512, and v_cache may equal k_cache (the
- * latent is the first 512 channels of each row). */
+ * (512 latent + 64 k_pe), head_dim_v = 512, and v_cache must equal k_cache with
+ * the same strides: the values are the first 512 (latent) channels of each
+ * cache row. */
 typedef struct pkv_attn_desc {
     int32_t dtype;          /* PKV_BF16 (MFMA path) or PKV_F32 (GQA only) */
     int32_t variant;        /* PKV_ATTN_GQA or PKV_ATTN_MLA */
@@ -207,7 +208,8 @@ size_t pkv_attention_workspace_size(const pkv_attn_desc* desc, int32_t n_q_heads
  * pkv_attention_workspace_size() bytes (may be NULL when that is 0), owned by
  * the caller, contents scratch.
  * Errors: PKV_ERR_NULL, PKV_ERR_SHAPE (n_q_heads % n_kv_heads != 0, sizes <= 0,
- * workspace too small, MLA shape not 576/512 with one KV head), PKV_ERR_ALIGN,
+ * workspace too small, MLA shape not 576/512 with one KV head or v_cache not
+ * k_cache), PKV_ERR_ALIGN,
  * PKV_ERR_UNSUPPORTED (head_dim other than 64 or 128 for GQA; fp32 MLA),
  * PKV_ERR_DEVICE. */
 pkv_status pkv_suffix_attention(const void* q, const void* k_cache, const void* v_cache, void* out,

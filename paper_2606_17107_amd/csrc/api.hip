@@ -176,6 +176,9 @@ pkv_status check_attention(const void* q, const void* k, const void* v, void* ou
         if (d->dtype != PKV_BF16) return fail(PKV_ERR_UNSUPPORTED, "MLA attention is bf16 only");
         if (Hkv != 1 || D != 576 || d->head_dim_v != 512)
             return fail(PKV_ERR_SHAPE, "MLA needs n_kv_heads 1, head_dim 576, head_dim_v 512");
+        if (v != k || memcmp(d->v_stride, d->k_stride, sizeof d->k_stride) != 0)
+            return fail(PKV_ERR_SHAPE, "MLA reads values from the latent channels of k_cache: v_cache must be "
+                                       "k_cache with the same strides");
     }
     const int eb = d->dtype == PKV_BF16 ? 2 : 4;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))

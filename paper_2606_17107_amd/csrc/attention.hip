@@ -7,6 +7,9 @@
 #ifndef PKV_ATTN_STAGES
 #define PKV_ATTN_STAGES 2      // LDS pipeline depth of the bf16 GQA kernel
 #endif
+#ifndef PKV_MLA_STAGES
+#define PKV_MLA_STAGES 4       // LDS pipeline depth of the MLA kernel
+#endif
 #ifndef PKV_ATTN_WAVES
 #define PKV_ATTN_WAVES 4       // waves per workgroup (8 selects the ping-pong schedule)
 #endif
@@ -14,6 +17,7 @@
 namespace pkv {
 
 hipError_t launch_attn_gqa_bf16(const AttnArgs& a, const Plan& p, dim3 grid, hipStream_t stream);
+hipError_t launch_attn_mla_bf16(const AttnArgs& a, const Plan& p, dim3 grid, hipStream_t stream);
 
 namespace {
 
@@ -150,22 +154,39 @@ Plan make_plan(const AttnArgs& a, int splits) {
     Plan p;
     p.G = a.n_heads / a.n_kv_heads;
     const int64_t m_rows = (int64_t)a.max_q * p.G;
-    // bf16 workgroup shape: 4 waves x 32 rows with a 2-stage LDS ring, so two
-    // independent workgroups share each CU and their MFMA and softmax phases
-    // interleave on every SIMD.
-    p.qb = 1;
-    p.nw = PKV_ATTN_WAVES;
-    p.ns = PKV_ATTN_STAGES;
-    p.BM = a.dtype == 1 ? 64 : p.nw * 32 * p.qb;
+    int tile = 64;
+    if (a.variant == 1) {
+        // MLA: 4 waves = 2 blocks of 32 rows x 2 output halves; 32-key tiles.
+        p.qb = 1;
+        p.nw = 4;
+        p.ns = PKV_MLA_STAGES;
+        tile = 32;
+    } else {
+        // bf16 GQA: 4 waves x 32 rows with a 2-stage LDS ring, so two
+        // independent workgroups share each CU and their MFMA and softmax
+        // phases interleave on every SIMD.
+        p.qb = 1;
+        p.nw = PKV_ATTN_WAVES;
+        p.ns = PKV_ATTN_STAGES;
+    }
+    p.BM = a.dtype == 1 ? 64 : (a.variant == 1 ? 64 : p.nw * 32 * p.qb);
     p.rbs = (int)((m_rows + p.BM - 1) / p.BM);
     if (p.rbs < 1) p.rbs = 1;
     p.splits = splits;
     p.n_groups = a.n_layers * a.n_kv_heads * a.n_seqs * splits;
-    const int tile = 64;
     int chunk = (a.max_kv_len + splits - 1) / splits;
     chunk = (chunk + tile - 1) / tile * tile;
     p.chunk = chunk < tile ? tile : chunk;
     return p;
+}
+
+// Workgroups that fit on one CU at once (LDS bound).
+int wgs_per_cu(const AttnArgs& a, const Plan& p) {
+    int lds;
+    if (a.variant == 1) lds = p.ns * 32 * 576 * 2;
+    else lds = (p.nw == 8 ? 4 : p.ns) * 2 * 64 * a.head_dim * 2;
+    const int n = (160 * 1024) / (lds > 0 ? lds : 1);
+    return n < 1 ? 1 : n;
 }
 
 }  // namespace
@@ -178,19 +199,25 @@ int attention_splits(const AttnArgs& a) {
         if (s > max_s) s = max_s < 1 ? 1 : max_s;
         return s;
     }
-    // Split the keys only as far as needed to give each of the 256 CUs as many
-    // workgroups as fit in its LDS at once, keeping at least 256 keys per split.
+    // Pick the split count that minimises the estimated time: workgroup rounds
+    // over the CUs divided by the split factor (each split does 1/s of the
+    // keys), with a small charge for the combine pass; at least 256 keys per
+    // split.
     const Plan p = make_plan(a, 1);
     const int64_t wgs = (int64_t)p.n_groups * p.rbs;
-    const int lds_per_wg = (p.nw == 8 ? 4 : p.ns) * 2 * 64 * a.head_dim * 2;
-    const int per_cu = lds_per_wg > 0 ? (160 * 1024) / lds_per_wg : 1;
-    const int64_t target = 256 * (int64_t)(per_cu < 1 ? 1 : per_cu);
-    int s = (int)((target + wgs - 1) / wgs);
-    const int max_s = a.max_kv_len / 256;
-    if (s > max_s) s = max_s;
-    if (s > 16) s = 16;
-    if (s < 1) s = 1;
-    return s;
+    const int64_t slots = 256 * (int64_t)wgs_per_cu(a, p);
+    int best = 1;
+    double best_t = 1e30;
+    for (int s = 1; s <= 8; ++s) {
+        if (s > 1 && a.max_kv_len / s < 256) break;
+        const double rounds = (double)((wgs * s + slots - 1) / slots);
+        const double t = rounds / s * (s > 1 ? 1.03 : 1.0);
+        if (t < best_t - 1e-9) {
+            best_t = t;
+            best = s;
+        }
+    }
+    return best;
 }
 
 size_t attention_workspace_bytes(const AttnArgs& a, int n_splits) {
@@ -200,7 +227,6 @@ size_t attention_workspace_bytes(const AttnArgs& a, int n_splits) {
 }
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
-    if (a.variant != 0) return hipErrorNotSupported;
     const Plan p = make_plan(a, a.n_splits < 1 ? 1 : a.n_splits);
     const int64_t groups_padded = ((int64_t)p.n_groups + kXcds - 1) / kXcds * kXcds;
     const int64_t n_wg = groups_padded * p.rbs;
@@ -214,7 +240,7 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
             hipLaunchKernelGGL((attn_gqa_f32<128>), grid, block, 0, stream, a, p);
         return hipGetLastError();
     }
-    hipError_t e = launch_attn_gqa_bf16(a, p, grid, stream);
+    hipError_t e = a.variant == 1 ? launch_attn_mla_bf16(a, p, grid, stream) : launch_attn_gqa_bf16(a, p, grid, stream);
     if (e != hipSuccess || p.splits == 1) return e;
     const int64_t threads = (int64_t)a.n_layers * a.total_q * a.n_heads * (a.head_dim_v / 4);
     dim3 cgrid((unsigned)((threads + 255) / 256));

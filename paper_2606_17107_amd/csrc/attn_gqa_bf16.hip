@@ -38,20 +38,6 @@ __device__ inline int swz(int key) { return ((key & 3) << 1) | ((key >> 2) & 1);
 // Scheduling pattern for the overlapped region (QK^T of the next tile next
 // to the probabilities of this one): per K-operand read, its two MFMAs
 // (32 cycles each) with about eight VALU instructions in their shadow.
-// Scheduling pattern for a run of N operand loads from LDS, R reads per
-// operand, each operand feeding Q MFMAs: the first two operands' reads go
-// first, then every MFMA group is followed by the reads of the operand two
-// steps ahead.  This bounds the registers held by prefetched operands.
-template <int N, int R, int Q>
-__device__ inline void sched_reads_mfma() {
-    __builtin_amdgcn_sched_group_barrier(0x100, 2 * R, 0);
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, Q, 0);
-        if (i + 2 < N) __builtin_amdgcn_sched_group_barrier(0x100, R, 0);
-    }
-}
-
 #ifndef PKV_ATTN_PINGPONG
 #define PKV_ATTN_PINGPONG 1
 #endif

@@ -1,0 +1,292 @@
+// bf16 MLA suffix attention (absorbed form) for gfx950.
+//
+// The MLA cache keeps, per token, one latent row [c_kv (512) | k_pe (64)]
+// shared by every head (paper Sec. 8, MLA adapter: a position-free latent
+// plus a small decoupled-RoPE sub-vector).  With absorbed queries
+// q = [q_latent (512) | q_pe (64)] per head, the scores run over all 576
+// channels and the values are the 512 latent channels of the same row:
+//     o_h = sum_j softmax_j(scale <q_h, row_j>) row_j[0:512]
+//
+// Work decomposition (one KV "head", so every query head is a row):
+//   * MFMA 32x32x16 bf16 -> fp32; row m <-> query m / H, head m % H.  Two
+//     waves share each block of 32 rows: both form the 576-channel scores
+//     (Q^T operand in VGPRs), each accumulates one 256-channel half of O^T
+//     (128 values per lane).  A full 512-channel O^T per wave would not fit
+//     the register file next to the Q^T operand.
+//   * S^T = K Q^T (36 k-steps), online softmax in-lane as in the GQA kernel,
+//     O^T += V^T P^T where V^T comes from the same LDS tile through
+//     ds_read_b64_tr_b16 (channels 0..511).
+//   * Tiles of 32 keys (36 KB) stream HBM -> LDS by LDS-DMA through NS
+//     stages; chunks XOR-swizzled by the key as in the GQA kernel.
+#include <type_traits>
+
+#include "attn_common.h"
+
+#ifndef PKV_MLA_STAGES
+#define PKV_MLA_STAGES 4
+#endif
+
+namespace pkv {
+namespace {
+
+constexpr int MBN = 32;        // keys per tile
+constexpr int DQK = 576;       // score channels
+constexpr int DV = 512;        // value (latent) channels
+constexpr int MCH = DQK / 8;   // 16-byte chunks per row: 72
+
+__device__ inline int mswz(int key) { return ((key & 3) << 1) | ((key >> 2) & 1); }
+
+template <int NS>
+__global__ __launch_bounds__(256) void attn_mla_bf16_kernel(AttnArgs a, Plan p) {
+    constexpr int NW = 4;
+    constexpr int PER = MBN * MCH / 64 / NW;   // LDS-DMA loads per wave per tile: 9
+    constexpr int KS = DQK / 16;               // 36
+    constexpr int DB = DV / 64;                // 32-channel blocks per wave (its half of DV): 8
+    constexpr int TE = MBN * DQK;              // elements per tile
+    static_assert(MBN * MCH % (64 * NW) == 0, "tile loads must split evenly over the waves");
+    static_assert(NS >= 2 && NS <= 4, "2..4 stages");
+
+    __shared__ __attribute__((aligned(16))) uint16_t t0_[TE], t1_[TE], t2_[NS > 2 ? TE : 8], t3_[NS > 3 ? TE : 8];
+    __shared__ int red[NW];
+    auto stage = [&](int st) -> uint16_t* { return st == 0 ? t0_ : st == 1 ? t1_ : st == 2 ? t2_ : t3_; };
+
+    int group, rb;
+    if (!decode(p, group, rb)) return;
+    const int split = group % p.splits;
+    int rest = group / p.splits;   // one KV head
+    const int layer = rest % a.n_layers;
+    const int seq = rest / a.n_layers;
+    const SeqInfo si = seq_info(a, seq);
+    const int H = a.n_heads;
+    const int M = si.nq * H;
+    const int m0 = rb * (NW / 2 * 32);
+    const int vhalf = (threadIdx.x >> 6) & 1;   // which 256-channel half of O this wave owns
+    if (m0 >= M) return;
+
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6;
+    const int lane = tid & 63;
+    const int j = lane & 31;
+    const int hl = lane >> 5;
+
+    const int m = m0 + (wave >> 1) * 32 + j;
+    const bool row_ok = m < M;
+    const int qi = row_ok ? m / H : 0;
+    const int head = row_ok ? m - qi * H : 0;
+    const int qpos = row_ok ? a.q_pos[si.q0 + qi] : -1;
+    const int row_end = row_ok ? max(0, min(si.kvl, qpos + 1)) : 0;
+    const int wmin = wave_min_i(row_ok ? row_end : 0x7fffffff);
+    const int wmax = wave_max_i(row_end);
+    if (lane == 0) red[wave] = wmax;
+    __syncthreads();
+    const int e_max = max(max(red[0], red[1]), max(red[2], red[3]));
+    const int k_begin = split * p.chunk;
+    const int loop_end = min(min(si.kvl, k_begin + p.chunk), e_max);
+    const int n_tiles = loop_end > k_begin ? (loop_end - k_begin + MBN - 1) / MBN : 0;
+
+    bf16x8 qf[KS];
+    {
+        const uint16_t* qrow = (const uint16_t*)a.q + (int64_t)layer * a.q_stride[0] +
+                               (int64_t)(si.q0 + qi) * a.q_stride[1] + (int64_t)head * a.q_stride[2];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            u32x4 v = {0u, 0u, 0u, 0u};
+            if (row_ok) v = *(const u32x4*)(qrow + ks * 16 + hl * 8);
+            qf[ks] = __builtin_bit_cast(bf16x8, v);
+        }
+    }
+
+    const uint16_t* kbase = (const uint16_t*)a.k + (int64_t)layer * a.k_stride[0] + si.base * a.k_stride[2];
+    const int64_t kss = a.k_stride[2];
+    const int last_key = loop_end - 1;
+    int32_t src_off[PER];
+    int key_of[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+        const int slot = (wave * PER + i) * 64 + lane;
+        key_of[i] = slot / MCH;
+        const int logical = (slot % MCH) ^ mswz(key_of[i]);
+        src_off[i] = (int32_t)((int64_t)key_of[i] * kss * 2 + logical * 16);
+    }
+    auto issue = [&](int t0, uint16_t* dst_stage) {
+        const bool full = t0 + MBN <= loop_end;
+        const char* kt = (const char*)(kbase + (int64_t)t0 * kss);
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            int32_t off = src_off[i];
+            if (!full) {
+                const int over = t0 + key_of[i] - last_key;
+                if (over > 0) off -= over * (int32_t)(kss * 2);
+            }
+            uint16_t* dst = dst_stage + (wave * PER + i) * 64 * 8;
+            __builtin_amdgcn_global_load_lds((const void*)(kt + off), PKV_LDS(void, dst), 16, 0, 0);
+        }
+    };
+
+    f32x16 o[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[db] = f32x16{};
+    float m_run = -INFINITY, l_run = 0.f;
+    const float sc2 = a.scale * kLog2e;
+    constexpr float kLazy = 8.0f;
+
+    auto compute = [&](int t0, const uint16_t* ts, auto mask_tag) {
+        constexpr bool MASK = decltype(mask_tag)::value;
+        // S^T = K Q^T over 576 channels, 32 keys.
+        f32x16 s = f32x16{};
+        const int key = j;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const int phys = (ks * 2 + hl) ^ mswz(key);
+            const u32x4 kv = *(const u32x4*)(ts + key * DQK + phys * 8);
+            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kv), qf[ks], s, 0, 0, 0);
+        }
+        sched_reads_mfma<KS, 1, 1>();
+        if (MASK) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int kk = t0 + (r >> 2) * 8 + hl * 4 + (r & 3);
+                if (kk >= row_end) s[r] = sc2 >= 0.f ? -INFINITY : INFINITY;
+            }
+        }
+        float mx;
+        if (sc2 >= 0.f) {
+            mx = -INFINITY;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[r]);
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+        } else {
+            mx = INFINITY;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) mx = fminf(mx, s[r]);
+            mx = fminf(mx, __shfl_xor(mx, 32));
+        }
+        const float msc = mx * sc2;
+        const bool up = msc > m_run + kLazy;
+        if (__builtin_amdgcn_ballot_w64(up) != 0) {
+            const float m_new = up ? msc : m_run;
+            const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+            l_run *= alpha;
+#pragma unroll
+            for (int db = 0; db < DB; ++db) o[db] *= alpha;
+            m_run = m_new;
+        }
+        const float neg_m = m_run == -INFINITY ? 0.f : -m_run;
+        float lsum = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            float e = __builtin_amdgcn_exp2f(fmaf(s[r], sc2, neg_m));
+            if (MASK) {
+                const int kk = t0 + (r >> 2) * 8 + hl * 4 + (r & 3);
+                if (kk >= row_end) e = 0.f;
+            }
+            s[r] = e;
+            lsum += e;
+        }
+        l_run += lsum;
+        bf16x8 pb[2];
+#pragma unroll
+        for (int st = 0; st < 2; ++st) {
+            f32x8 pv;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) pv[e] = s[st * 8 + e];
+            pb[st] = __builtin_convertvector(pv, bf16x8);
+        }
+        // O^T += V^T P^T: V is channels 0..511 of the same tile.
+        const int g = lane >> 4, sl = lane & 15;
+        const int hh = g >> 1;
+#pragma unroll
+        for (int st = 0; st < 2; ++st) {
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                s16x4 part[2];
+#pragma unroll
+                for (int b = 0; b < 2; ++b) {
+                    const int kk = st * 16 + b * 8 + hh * 4 + (sl >> 2);
+                    const int col = vhalf * 256 + db * 32 + (g & 1) * 16 + (sl & 3) * 4;
+                    const int phys = (col >> 3) ^ mswz(kk);
+                    part[b] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                        PKV_LDS(s16x4, ts + kk * DQK + phys * 8 + (col & 7)));
+                }
+                const s16x4 p0 = part[0], p1 = part[1];
+                const bf16x8 vf = __builtin_bit_cast(
+                    bf16x8, (short __attribute__((ext_vector_type(8)))){p0[0], p0[1], p0[2], p0[3], p1[0], p1[1],
+                                                                          p1[2], p1[3]});
+                o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[st], o[db], 0, 0, 0);
+            }
+        }
+        sched_reads_mfma<2 * DB, 2, 1>();
+    };
+
+    auto wait_outstanding = [&](int tiles_after) {
+        if (NS > 3 && tiles_after >= 3) wait_vmcnt<(NS > 3 ? 3 : 1) * PER>();
+        else if (NS > 2 && tiles_after >= 2) wait_vmcnt<(NS > 2 ? 2 : 1) * PER>();
+        else if (tiles_after == 1) wait_vmcnt<PER>();
+        else wait_vmcnt<0>();
+    };
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+        if (s < n_tiles) issue(k_begin + s * MBN, stage(s));
+    for (int t = 0; t < n_tiles; t += NS) {
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            const int i = t + s;
+            if (i < n_tiles) {
+                const int ahead = i + NS - 1;
+                if (ahead < n_tiles) issue(k_begin + ahead * MBN, stage((s + NS - 1) % NS));
+                wait_outstanding(min(ahead, n_tiles - 1) - i);
+                bare_barrier();
+                const int t0 = k_begin + i * MBN;
+                if (t0 + MBN > wmin)
+                    compute(t0, stage(s), std::true_type{});
+                else
+                    compute(t0, stage(s), std::false_type{});
+                __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
+                bare_barrier();
+            }
+        }
+    }
+
+    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    if (!row_ok) return;
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const float lse2 = l_tot > 0.f ? m_run + __log2f(l_tot) : -INFINITY;
+    const int64_t row = si.q0 + qi;
+    if (p.splits == 1) {
+        uint16_t* orow = (uint16_t*)a.out + (int64_t)layer * a.o_stride[0] + row * a.o_stride[1] +
+                         (int64_t)head * a.o_stride[2];
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                u32x2 w;
+                w[0] = bf_rne(o[db][4 * b] * inv) | (bf_rne(o[db][4 * b + 1] * inv) << 16);
+                w[1] = bf_rne(o[db][4 * b + 2] * inv) | (bf_rne(o[db][4 * b + 3] * inv) << 16);
+                *(u32x2*)(orow + vhalf * 256 + db * 32 + b * 8 + hl * 4) = w;
+            }
+        }
+        if (a.lse_out && hl == 0 && vhalf == 0) a.lse_out[((int64_t)layer * a.total_q + row) * H + head] = lse2 * kLn2;
+    } else {
+        const int64_t item = (((int64_t)split * a.n_layers + layer) * a.total_q + row) * H + head;
+        float* wo = a.ws_o + item * DV;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                f32x4 w = {o[db][4 * b] * inv, o[db][4 * b + 1] * inv, o[db][4 * b + 2] * inv,
+                           o[db][4 * b + 3] * inv};
+                *(f32x4*)(wo + vhalf * 256 + db * 32 + b * 8 + hl * 4) = w;
+            }
+        }
+        if (hl == 0 && vhalf == 0) a.ws_lse[item] = lse2;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_attn_mla_bf16(const AttnArgs& a, const Plan& p, dim3 grid, hipStream_t stream) {
+    hipLaunchKernelGGL((attn_mla_bf16_kernel<PKV_MLA_STAGES>), grid, dim3(256), 0, stream, a, p);
+    return hipGetLastError();
+}
+
+}  // namespace pkv

@@ -150,6 +150,7 @@ def attend(d, H=32, Hkv=8, D=128, q=Q, k=K, v=V, o=O, qp=QP, kl=KL, ws=None, wsb
     (dict(head_dim_v=64), {}, pkv.PKV_ERR_SHAPE),
     (dict(variant=1), {}, pkv.PKV_ERR_SHAPE),                 # MLA needs 1 KV head, 576/512
     (dict(variant=1, dtype=1, head_dim_v=512), dict(Hkv=1, D=576), pkv.PKV_ERR_UNSUPPORTED),
+    (dict(variant=1, head_dim_v=512), dict(Hkv=1, D=576), pkv.PKV_ERR_SHAPE),   # MLA values must come from k_cache
     (dict(dtype=5), {}, pkv.PKV_ERR_UNSUPPORTED),
     ({}, dict(o=O + 8), pkv.PKV_ERR_ALIGN),
     (dict(q_stride=pkv._i64x3(64 * 32 * 128, 32 * 128, 100)), {}, pkv.PKV_ERR_ALIGN),

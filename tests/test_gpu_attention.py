@@ -240,3 +240,93 @@ def test_full_gqa8b():
 def test_full_long32k_sampled():
     rows = np.unique(np.concatenate([[0, 1, 511, 1022, 1023], np.random.default_rng(0).integers(0, 1024, 11)]))
     full_gqa(synth.LONG32K, layers=[0, 27], rows=rows)
+
+
+# ---- MLA (absorbed form; Sec. 8 MLA adapter) ----------------------------------
+
+def mla_case(L, H, n_q, kv, seed):
+    g = synth.Draws(seed, "cpu")
+    q = host_bits(g.normal((L, n_q, H, 576)))
+    rows = host_bits(g.normal((L, 1, kv, 576)))
+    q_pos = np.arange(kv - n_q, kv, dtype=np.int32)
+    return q, rows, q_pos
+
+
+def gpu_mla(q, rows, q_pos, kv, scale, splits=0, lse=False):
+    qd, rd = dev(q), dev(rows)
+    L, n_q, H = q.shape[:3]
+    out = torch.zeros(L, n_q, H, 512, dtype=torch.bfloat16, device="cuda")
+    lse_t = torch.zeros(L, n_q, H, dtype=torch.float32, device="cuda") if lse else None
+    pkv.suffix_attention(qd, rd, rd[..., :512], out, torch.from_numpy(q_pos).cuda(),
+                         torch.tensor([kv], dtype=torch.int32, device="cuda"), scale, max_kv_len=kv,
+                         variant=pkv.PKV_ATTN_MLA, n_splits=splits, lse_out=lse_t)
+    torch.cuda.synchronize()
+    return (host_bits(out), lse_t.cpu().numpy()) if lse else host_bits(out)
+
+
+@pytest.mark.parametrize("splits", [1, 3, 0])
+def test_mla_small(splits):
+    L, H, n_q, kv = 2, 16, 9, 700
+    q, rows, q_pos = mla_case(L, H, n_q, kv, 8)
+    q_pos[0] = 10                                   # one row near the start of the cache
+    scale = 1 / math.sqrt(192)
+    got, lse = gpu_mla(q, rows, q_pos, kv, scale, splits, lse=True)
+    for l in range(L):
+        want, wl = oracle.attention(q[l], rows[l], rows[l][..., :512], q_pos, kv, scale)
+        log("  mla splits=%d layer %d" % (splits, l), check_attention_close(got[l], want))
+        np.testing.assert_allclose(lse[l], wl, atol=2e-2)
+
+
+def test_mla_sharpened():
+    L, H, n_q, kv = 1, 16, 6, 400
+    q, rows, q_pos = mla_case(L, H, n_q, kv, 9)
+    q4 = synth.to_numpy_bits(synth.from_numpy_bits(q).float().mul(4).to(torch.bfloat16))
+    scale = 1 / math.sqrt(192)
+    got = gpu_mla(q4, rows, q_pos, kv, scale, 2)
+    want, _ = oracle.attention(q4[0], rows[0], rows[0][..., :512], q_pos, kv, scale)
+    log("  mla sharpened", check_attention_close(got[0], want))
+
+
+def test_mla_splice_then_attend():
+    """MLA end to end: rotate only k_pe of a skill's latent rows into the cache, then absorbed attention,
+    against the oracle doing both steps."""
+    w = synth.Workload("mla_small", 2, 16, 1, 576, 512, 1e4, 64, 512, synth.INTERLEAVED, "bf16", 300, 0, 200, 800,
+                       12, 1 / math.sqrt(192), mla=True)
+    c = synth.gqa_case(w, seed=10)
+    src, dst, q_pos = c["src_pos"].numpy(), c["dst_pos"].numpy(), c["q_pos"].numpy()
+    skill = rope_cache(host_bits(c["skill_k_pre"]), src[None, None, :], w)
+    cache = host_bits(c["ctx_k"])
+    q = host_bits(c["q_pre"])
+    kd = dev(cache)
+    pkv.reposition_splice(dev(skill), None, kd, None, c["src_pos"].cuda(), c["dst_pos"].cuda(), w.theta, w.rope_dim,
+                          w.rope_offset, w.rope_style)
+    out = torch.zeros(2, w.n_q, w.n_heads, 512, dtype=torch.bfloat16, device="cuda")
+    pkv.suffix_attention(dev(q), kd, kd[..., :512], out, c["q_pos"].cuda(),
+                         torch.tensor([w.kv_len], dtype=torch.int32, device="cuda"), w.scale, max_kv_len=w.kv_len,
+                         variant=pkv.PKV_ATTN_MLA)
+    torch.cuda.synchronize()
+    ref_cache = cache.copy()
+    oracle.reposition_splice(skill, None, ref_cache, None, src, dst, w.theta, w.rope_dim, w.rope_offset, w.rope_style)
+    got = host_bits(out)
+    for l in range(2):
+        want, _ = oracle.attention(q[l], ref_cache[l], ref_cache[l][..., :512], q_pos, w.kv_len, w.scale)
+        check_attention_close(got[l], want)
+
+
+def test_full_mla_sampled():
+    w = synth.MLA
+    c = synth.gqa_case(w, seed=0, device="cuda")
+    q, k = c["q_pre"], c["ctx_k"]
+    out = torch.zeros(w.n_layers, w.n_q, w.n_heads, 512, dtype=torch.bfloat16, device="cuda")
+    log("full-size MLA attention")
+    pkv.suffix_attention(q, k, k[..., :512], out, c["q_pos"].cuda(),
+                         torch.tensor([w.kv_len], dtype=torch.int32, device="cuda"), w.scale, max_kv_len=w.kv_len,
+                         variant=pkv.PKV_ATTN_MLA)
+    torch.cuda.synchronize()
+    rows = np.array([0, 1, 63, 126, 127])
+    for layer in (0, 26):
+        qh = host_bits(q[layer])[rows]
+        kh = host_bits(k[layer])
+        want, _ = oracle.attention(np.ascontiguousarray(qh), kh, kh[..., :512], c["q_pos"].numpy()[rows], w.kv_len,
+                                   w.scale)
+        log("  layer", layer, check_attention_close(host_bits(out[layer])[rows], want))
