@@ -347,17 +347,20 @@ __global__ __launch_bounds__(NW * 64, NW == 4 && NS == 2 ? 2 : 1) void attn_gqa_
     for (int s = 0; s < (PIPE ? 1 : NS - 1); ++s)
         if (s < n_tiles) issue(k_begin + s * BN, kst(s), vst(s));
     if constexpr (!PIPE) {
-        // Plain order: tile i is waited for, then QK^T, softmax and PV run back to back.
+        // Plain order: tile i is waited for, then QK^T, softmax and PV run back
+        // to back.  The barrier that publishes tile i also proves every wave
+        // finished tile i-1, so tile i-1's stage is refilled right after it.
         for (int t = 0; t < n_tiles; t += NS) {
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
                 const int i = t + s;
                 if (i < n_tiles) {
+                    wait_outstanding(min(i + NS - 2, n_tiles - 1) - i);
+                    __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
+                    bare_barrier();
                     const int ahead = i + NS - 1;
                     if (ahead < n_tiles)
                         issue(k_begin + ahead * BN, kst((s + NS - 1) % NS), vst((s + NS - 1) % NS));
-                    wait_outstanding(min(ahead, n_tiles - 1) - i);
-                    bare_barrier();
                     f32x16 sc[2][QB];
                     qk(kst(s), sc);
                     bf16x8 pb[QB][4];
@@ -370,8 +373,6 @@ __global__ __launch_bounds__(NW * 64, NW == 4 && NS == 2 ? 2 : 1) void attn_gqa_
                         probs(t0, sc, pb, std::false_type{});
                     }
                     pv(vst(s), pb);
-                    __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
-                    bare_barrier();
                 }
             }
         }

@@ -9,10 +9,11 @@
 //
 // Work decomposition (one KV "head", so every query head is a row):
 //   * MFMA 32x32x16 bf16 -> fp32; row m <-> query m / H, head m % H.  Two
-//     waves share each block of 32 rows: both form the 576-channel scores
-//     (Q^T operand in VGPRs), each accumulates one 256-channel half of O^T
-//     (128 values per lane).  A full 512-channel O^T per wave would not fit
-//     the register file next to the Q^T operand.
+//     waves share each block of 32 rows.  Each forms the partial scores over
+//     one half of the 576 channels (its Q^T half, 72 VGPRs, in registers),
+//     the two partials are exchanged through LDS and added (fp32), both waves
+//     run the same online softmax, and each accumulates one 256-channel half
+//     of O^T (128 values per lane).
 //   * S^T = K Q^T (36 k-steps), online softmax in-lane as in the GQA kernel,
 //     O^T += V^T P^T where V^T comes from the same LDS tile through
 //     ds_read_b64_tr_b16 (channels 0..511).
@@ -23,7 +24,7 @@
 #include "attn_common.h"
 
 #ifndef PKV_MLA_STAGES
-#define PKV_MLA_STAGES 4
+#define PKV_MLA_STAGES 2
 #endif
 
 namespace pkv {
@@ -40,7 +41,7 @@ template <int NS>
 __global__ __launch_bounds__(256) void attn_mla_bf16_kernel(AttnArgs a, Plan p) {
     constexpr int NW = 4;
     constexpr int PER = MBN * MCH / 64 / NW;   // LDS-DMA loads per wave per tile: 9
-    constexpr int KS = DQK / 16;               // 36
+    constexpr int KS = DQK / 16 / 2;           // k-steps per wave (its half of the channels): 18
     constexpr int DB = DV / 64;                // 32-channel blocks per wave (its half of DV): 8
     constexpr int TE = MBN * DQK;              // elements per tile
     static_assert(MBN * MCH % (64 * NW) == 0, "tile loads must split evenly over the waves");
@@ -48,6 +49,8 @@ __global__ __launch_bounds__(256) void attn_mla_bf16_kernel(AttnArgs a, Plan p) 
 
     __shared__ __attribute__((aligned(16))) uint16_t t0_[TE], t1_[TE], t2_[NS > 2 ? TE : 8], t3_[NS > 3 ? TE : 8];
     __shared__ int red[NW];
+    // Partial-score exchange: [wave][4 chunks][64 lanes] x 16 bytes.
+    __shared__ __attribute__((aligned(16))) float xch[NW * 4 * 64 * 4];
     auto stage = [&](int st) -> uint16_t* { return st == 0 ? t0_ : st == 1 ? t1_ : st == 2 ? t2_ : t3_; };
 
     int group, rb;
@@ -91,7 +94,7 @@ __global__ __launch_bounds__(256) void attn_mla_bf16_kernel(AttnArgs a, Plan p) 
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             u32x4 v = {0u, 0u, 0u, 0u};
-            if (row_ok) v = *(const u32x4*)(qrow + ks * 16 + hl * 8);
+            if (row_ok) v = *(const u32x4*)(qrow + (vhalf * KS + ks) * 16 + hl * 8);
             qf[ks] = __builtin_bit_cast(bf16x8, v);
         }
     }
@@ -132,16 +135,38 @@ __global__ __launch_bounds__(256) void attn_mla_bf16_kernel(AttnArgs a, Plan p) 
 
     auto compute = [&](int t0, const uint16_t* ts, auto mask_tag) {
         constexpr bool MASK = decltype(mask_tag)::value;
-        // S^T = K Q^T over 576 channels, 32 keys.
-        f32x16 s = f32x16{};
+        // Partial S^T = K Q^T over this wave's 288 channels, 32 keys, in two
+        // independent accumulation chains.
+        f32x16 sa = f32x16{}, sb = f32x16{};
         const int key = j;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-            const int phys = (ks * 2 + hl) ^ mswz(key);
+            const int phys = ((vhalf * KS + ks) * 2 + hl) ^ mswz(key);
             const u32x4 kv = *(const u32x4*)(ts + key * DQK + phys * 8);
-            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kv), qf[ks], s, 0, 0, 0);
+            if (ks & 1)
+                sb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kv), qf[ks], sb, 0, 0, 0);
+            else
+                sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kv), qf[ks], sa, 0, 0, 0);
         }
         sched_reads_mfma<KS, 1, 1>();
+        f32x16 s = sa + sb;
+        // Exchange the partial scores with the other wave of the pair (the
+        // lanes of both waves hold the same (key, row) elements).
+        float* mine = xch + wave * 1024;
+        const float* other = xch + (wave ^ 1) * 1024;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            *(f32x4*)(mine + (c * 64 + lane) * 4) = f32x4{s[4 * c], s[4 * c + 1], s[4 * c + 2], s[4 * c + 3]};
+        __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
+        bare_barrier();
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const f32x4 x = *(const f32x4*)(other + (c * 64 + lane) * 4);
+            s[4 * c] += x[0];
+            s[4 * c + 1] += x[1];
+            s[4 * c + 2] += x[2];
+            s[4 * c + 3] += x[3];
+        }
         if (MASK) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
@@ -226,23 +251,26 @@ __global__ __launch_bounds__(256) void attn_mla_bf16_kernel(AttnArgs a, Plan p) 
     };
 #pragma unroll
     for (int s = 0; s < NS - 1; ++s)
-        if (s < n_tiles) issue(k_begin + s * MBN, stage(s));
+        if (s < n_tiles) issue(k_begin + s * MBN, stage(s));   // tiles 0 .. NS-2
+    // Stage i % NS holds tile i.  Each iteration waits for tile i, then (after
+    // the barrier, when every wave has finished tile i-1) refills tile i-1's
+    // stage with tile i+NS-1.
     for (int t = 0; t < n_tiles; t += NS) {
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
             const int i = t + s;
             if (i < n_tiles) {
+                const int issued = min(i + NS - 2, n_tiles - 1);   // last tile already in flight
+                wait_outstanding(issued - i);
+                __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
+                bare_barrier();
                 const int ahead = i + NS - 1;
                 if (ahead < n_tiles) issue(k_begin + ahead * MBN, stage((s + NS - 1) % NS));
-                wait_outstanding(min(ahead, n_tiles - 1) - i);
-                bare_barrier();
                 const int t0 = k_begin + i * MBN;
                 if (t0 + MBN > wmin)
                     compute(t0, stage(s), std::true_type{});
                 else
                     compute(t0, stage(s), std::false_type{});
-                __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
-                bare_barrier();
             }
         }
     }
