@@ -105,62 +105,125 @@ class GqaStep:
         return self.w.attn_bytes()
 
 
-def cpu_baseline(w: synth.Workload, budget_s: float = 20.0):
-    """Time the fp64 oracle on a bounded sample of the same workload on the host cores."""
+def cpu_baseline(w: synth.Workload, budget_s: float = 10.0):
+    """Time the fp64 oracle on a bounded sample of the same workload on the host cores.
+
+    Splice: the full skill (all tokens) over as many layers as fit in about half
+    the budget.  Attention: layer 0, as many suffix queries as fit in the other
+    half, scaled to all layers and queries by visible (query, key) pairs."""
     import numpy as np
 
     import oracle
 
     oracle.build(force=False)
     threads = oracle.max_threads()
-    # splice sample: all tokens of the skill, a subset of layers
-    L_s = max(1, min(w.n_layers, 8))
-    c = synth.gqa_case(w, seed=1, layers=L_s)
     bits = synth.to_numpy_bits
-    sk, dk = bits(c["skill_k_pre"]), bits(c["ctx_k"])
-    sv = bits(c["skill_v"]) if "skill_v" in c else None
-    dv = bits(c["ctx_v"]) if "ctx_v" in c else None
-    src, dst = c["src_pos"].numpy(), c["dst_pos"].numpy()
+    # splice: time one layer first, then size the sample
+    c1 = synth.gqa_case(w, seed=1, layers=1)
+    one = dict(sk=bits(c1["skill_k_pre"]), dk=bits(c1["ctx_k"]),
+               sv=bits(c1["skill_v"]) if "skill_v" in c1 else None, dv=bits(c1["ctx_v"]) if "ctx_v" in c1 else None)
+    src, dst = c1["src_pos"].numpy(), c1["dst_pos"].numpy()
+
+    def run_splice(x):
+        oracle.reposition_splice(x["sk"], x["sv"], x["dk"], x["dv"], src, dst, w.theta, w.rope_dim, w.rope_offset,
+                                 w.rope_style)
+
     t0 = time.perf_counter()
-    oracle.reposition_splice(sk, sv, dk, dv, src, dst, w.theta, w.rope_dim, w.rope_offset, w.rope_style)
+    run_splice(one)
+    t_one = time.perf_counter() - t0
+    reps = max(1, min(64 * w.n_layers, int(0.5 * budget_s / max(t_one, 1e-4))))
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        run_splice(one)
     t_splice = time.perf_counter() - t0
-    sample_bytes = w.splice_bytes() * L_s / w.n_layers
-    # attention sample: one layer, a subset of queries, scaled by flops
-    q = bits(c["q_pre"][0])
-    k = dk[0]
-    v = dk[0][..., : w.v_dim] if w.mla else dv[0]
-    q_pos = c["q_pos"].numpy()
-    n_rows = w.n_q
-    est = w.attn_flops() / w.n_layers / 2e9 / max(threads, 1)   # ~2 GFLOP/s per core
-    if est > budget_s:
-        n_rows = max(1, int(w.n_q * budget_s / est))
+    sample_bytes = w.splice_bytes() / w.n_layers * reps
+    # attention: layer 0 of the same draws
+    q = bits(c1["q_pre"][0])
+    k = one["dk"][0]
+    v = k[..., : w.v_dim] if w.mla else one["dv"][0]
+    q_pos = c1["q_pos"].numpy()
     t0 = time.perf_counter()
-    oracle.attention(np.ascontiguousarray(q[:n_rows]), k, v, q_pos[:n_rows], w.kv_len, w.scale)
+    oracle.attention(np.ascontiguousarray(q[:1]), k, v, q_pos[:1], w.kv_len, w.scale)
+    t_row = max(time.perf_counter() - t0, 1e-4)
+    n_rows = max(1, min(w.n_q, int(0.5 * budget_s / t_row)))
+    # when every query of a layer fits, repeat the layer (up to the layer count) to fill the budget
+    passes = 1
+    if n_rows == w.n_q:
+        passes = max(1, min(w.n_layers, int(0.5 * budget_s / (t_row * w.n_q))))
+    t0 = time.perf_counter()
+    for _ in range(passes):
+        oracle.attention(np.ascontiguousarray(q[:n_rows]), k, v, q_pos[:n_rows], w.kv_len, w.scale)
     t_attn = time.perf_counter() - t0
     vis = sum(min(w.kv_len, int(q_pos[i]) + 1) for i in range(n_rows))
     vis_all = sum(min(w.kv_len, int(q_pos[i]) + 1) for i in range(w.n_q))
-    attn_us_full = t_attn * (vis_all / vis) * w.n_layers * 1e6
+    attn_us_full = t_attn / passes * (vis_all / vis) * w.n_layers * 1e6
     return {
         "value": round(sample_bytes / t_splice / 1e9, 4),
         "unit": "GB/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": "splice: all %d skill tokens x %d of %d layers (%.3f GB in %.2f s); attention: layer 0, "
-                  "%d of %d queries (%.2f s), extrapolated to all layers and queries"
-                  % (w.skill_tokens, L_s, w.n_layers, sample_bytes / 1e9, t_splice, n_rows, w.n_q, t_attn),
+        "sample": "splice: %d passes of one layer (all %d skill tokens, %.3f GB moved) in %.2f s; attention: "
+                  "%d pass(es) of layer 0, %d of %d queries over %d slots, in %.2f s, scaled to all layers and queries"
+                  % (reps, w.skill_tokens, sample_bytes / 1e9, t_splice, passes, n_rows, w.n_q, w.kv_len, t_attn),
         "attention_us_extrapolated": round(attn_us_full, 1),
     }
+
+
+def source_hash(files):
+    """Hash of the kernel sources a counter measurement was taken against."""
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+KERNEL_SOURCES = {
+    "splice_kernel": ["paper_2606_17107_amd/csrc/splice.hip"],
+    "attn_gqa_bf16": ["paper_2606_17107_amd/csrc/attn_gqa_bf16.hip", "paper_2606_17107_amd/csrc/attn_common.h"],
+    "attn_mla_bf16": ["paper_2606_17107_amd/csrc/attn_mla_bf16.hip", "paper_2606_17107_amd/csrc/attn_common.h"],
+}
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE record
+    (profiles/traffic.json), scaled by the plain-copy calibration; None when no record
+    exists or the kernel source changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    r = rec.get("kernels", {}).get(kernel, {}).get(workload)
+    if not r or r.get("source_hash") != source_hash(KERNEL_SOURCES[kernel]):
+        return None
+    return int(r["hbm_bytes_per_launch"])
+
+
+def copy_calibration():
+    """A plain device copy of a known size, for calibrating the FETCH_SIZE / WRITE_SIZE counters."""
+    n = 1 << 30
+    x = torch.ones(n, dtype=torch.uint8, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": n, "copy_calibration_bytes_written": n, "launches": 3}))
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--workload", default="gqa8b", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--splits", type=int, default=0, help="KV splits for attention (0 = library choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--cpu-budget", type=float, default=10.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a 1 GiB device copy (counter calibration for rocprofv3)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -169,6 +232,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
     pkv.lib()   # fail loudly if libpkv.so is missing
 
     w = synth.WORKLOADS[args.workload]
@@ -197,8 +263,11 @@ def main():
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
     total_ms = start.elapsed_time(stop)
-    splice_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
-    attn_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
+    splice_t = sorted(e[0].elapsed_time(e[1]) for e in ev)
+    attn_t = sorted(e[1].elapsed_time(e[2]) for e in ev)
+    # The mean launch duration is the figure rocprofv3's per-kernel average reports; median and min beside it.
+    splice_ms = sum(splice_t) / args.steps
+    attn_ms = sum(attn_t) / args.steps
     ms_per_step = total_ms / args.steps
 
     splice_gbs = step.splice_bytes() / (splice_ms * 1e-3) / 1e9
@@ -217,6 +286,11 @@ def main():
                    "frac": round(splice_gbs / HBM_PEAK_GBS, 4), "traffic": None}
     splice_roof["kernel"] = "splice_kernel"
     attn_roof["kernel"] = "attn_gqa_bf16" if not w.mla else "attn_mla_bf16"
+    splice_roof["traffic"] = measured_traffic("splice_kernel", w.name)
+    attn_roof["traffic"] = measured_traffic(attn_roof["kernel"], w.name)
+    splice_roof["algorithmic_bytes"] = step.splice_bytes()
+    attn_roof["algorithmic_bytes"] = step.attn_bytes()
+    attn_roof["algorithmic_flops"] = step.attn_flops()
     dominant = splice_roof if splice_ms >= attn_ms else attn_roof
 
     result = {
@@ -242,9 +316,11 @@ def main():
             "attention_splits": int(step.desc.n_splits) or "auto",
             "workspace_bytes": step.ws_bytes,
         },
-        "splice": {"us": round(splice_ms * 1e3, 2), "gbps": round(splice_gbs, 1)},
-        "attention": {"us": round(attn_ms * 1e3, 2), "tflops": round(attn_tflops, 2), "gbps": round(attn_gbs, 1),
-                      "arith_intensity": round(ai, 1), "bound": attn_bound},
+        "splice": {"us": round(splice_ms * 1e3, 2), "us_median": round(splice_t[len(splice_t) // 2] * 1e3, 2),
+                   "us_min": round(splice_t[0] * 1e3, 2), "gbps": round(splice_gbs, 1)},
+        "attention": {"us": round(attn_ms * 1e3, 2), "us_median": round(attn_t[len(attn_t) // 2] * 1e3, 2),
+                      "us_min": round(attn_t[0] * 1e3, 2), "tflops": round(attn_tflops, 2),
+                      "gbps": round(attn_gbs, 1), "arith_intensity": round(ai, 1), "bound": attn_bound},
         "roofline": dominant,
         "roofline_kernels": [splice_roof, attn_roof],
         "wall_s_timed": round(t_wall, 3),
