@@ -4,14 +4,11 @@
 // The bf16 GQA kernel lives in attn_gqa_bf16.hip.
 #include "attn_common.h"
 
-#ifndef PKV_ATTN_STAGES
-#define PKV_ATTN_STAGES 2      // LDS pipeline depth of the bf16 GQA kernel
+#ifndef PKV_ATTN_SHAPE
+#define PKV_ATTN_SHAPE 1       // bf16 GQA kernel: 0 plain order (64-key tiles), 1 pipelined (32-key tiles)
 #endif
 #ifndef PKV_MLA_STAGES
 #define PKV_MLA_STAGES 2       // LDS pipeline depth of the MLA kernel
-#endif
-#ifndef PKV_ATTN_WAVES
-#define PKV_ATTN_WAVES 4       // waves per workgroup (8 selects the ping-pong schedule)
 #endif
 
 namespace pkv {
@@ -162,12 +159,12 @@ Plan make_plan(const AttnArgs& a, int splits) {
         p.ns = PKV_MLA_STAGES;
         tile = 32;
     } else {
-        // bf16 GQA: 4 waves x 32 rows with a 2-stage LDS ring, so two
-        // independent workgroups share each CU and their MFMA and softmax
-        // phases interleave on every SIMD.
+        // bf16 GQA: 4 waves x 32 rows, two workgroups per CU; pipelined over
+        // 32-key tiles in 4 LDS stages, or plain order over 64-key tiles in 2.
         p.qb = 1;
-        p.nw = PKV_ATTN_WAVES;
-        p.ns = PKV_ATTN_STAGES;
+        p.nw = 4;
+        p.ns = PKV_ATTN_SHAPE == 1 ? 4 : 2;
+        tile = PKV_ATTN_SHAPE == 1 ? 32 : 64;
     }
     p.BM = a.dtype == 1 ? 64 : (a.variant == 1 ? 64 : p.nw * 32 * p.qb);
     p.rbs = (int)((m_rows + p.BM - 1) / p.BM);
@@ -184,7 +181,7 @@ Plan make_plan(const AttnArgs& a, int splits) {
 int wgs_per_cu(const AttnArgs& a, const Plan& p) {
     int lds;
     if (a.variant == 1) lds = p.ns * 32 * 576 * 2 + 16 * 1024;
-    else lds = (p.nw == 8 ? 4 : p.ns) * 2 * 64 * a.head_dim * 2;
+    else lds = p.ns * 2 * (p.ns == 4 ? 32 : 64) * a.head_dim * 2;
     const int n = (160 * 1024) / (lds > 0 ? lds : 1);
     return n < 1 ? 1 : n;
 }

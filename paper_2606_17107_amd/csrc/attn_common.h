@@ -4,11 +4,14 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 #include "pkv_internal.h"
 
 namespace pkv {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -88,6 +91,45 @@ __device__ inline uint32_t bf_rne(float f) {
     uint32_t u = __float_as_uint(f);
     u += 0x7fffu + ((u >> 16) & 1u);
     return u >> 16;
+}
+
+// One 16-byte LDS-DMA load per lane (global_load_lds_dwordx4, saddr form):
+// lane l's 16 bytes at sbase + voff[l] land at LDS byte address lds_addr +
+// 16*l; lds_addr (M0) and sbase are wave-uniform.  Written as inline assembly
+// so that the compiler does not see an LDS write in flight: with the builtin
+// it would wait for every outstanding LDS read (lgkmcnt 0) wherever it needs
+// any one of them.  Completion is tracked by the kernels themselves with
+// explicit vmcnt waits before the barrier that publishes a stage; the memory
+// clobber keeps LDS accesses on their side.  One wait state separates the M0
+// write from the load that reads it.
+// A wave-uniform 64-bit value in scalar registers.  readfirstlane returns a
+// signed int: each half is taken as uint32_t before widening.
+__device__ inline uint64_t uniform_u64(uint64_t v) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+#ifndef PKV_LDS_DMA16
+__device__ inline void lds_dma_asm(uint32_t m0, uint64_t sbase, uint32_t voff) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(m0), "v"(voff), "s"(sbase)
+                 : "memory");
+}
+
+// LDS byte address of a pointer into a __shared__ array (the low 32 bits of
+// its flat address).
+__device__ inline uint32_t lds_addr_of(const void* p) { return (uint32_t)(uintptr_t)p; }
+#endif
+__device__ inline void lds_dma16(uint32_t lds_addr, const void* sbase, uint32_t voff) {
+    lds_dma_asm((uint32_t)__builtin_amdgcn_readfirstlane(lds_addr), uniform_u64((uint64_t)(uintptr_t)sbase), voff);
+}
+
+// Compile-time loop: f(std::integral_constant<int, I>) for I = B .. E-1.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
 }
 
 // Wait until at most N vector-memory operations of this wave are outstanding

@@ -14,7 +14,7 @@
 //   * K and V tiles of 64 keys stream HBM -> LDS with LDS-DMA loads
 //     (global_load_lds, 16 bytes per lane) through NS stages, so NS-1 tiles
 //     are in flight while one is consumed.  16-byte chunks of a row are
-//     XOR-swizzled by swz(key) (below) to spread LDS banks.
+//     XOR-swizzled by key (swz_k / swz_v below) to spread LDS banks.
 //   * V stays row-major ([key][channel]) in LDS; the transposed A operand of
 //     the PV product comes from ds_read_b64_tr_b16, with the keys of each
 //     16-key step ordered as the P^T accumulator holds them.
@@ -25,57 +25,58 @@
 namespace pkv {
 namespace {
 
-constexpr int BN = 64;   // keys per tile
 
-// XOR swizzle of a row's 16-byte chunk index by its key (3 bits).  K operand
-// reads take one logical chunk from 8 consecutive keys: swz maps keys 0..7
-// to 0,2,4,6,1,3,5,7, all distinct, so they hit 8 distinct bank groups.  The
-// transposed V reads take two adjacent chunks (c, c+1; c even) from 4
-// consecutive keys 4m..4m+3: swz gives 2r (+1), so the four rows land on four
-// distinct chunk pairs.
-__device__ inline int swz(int key) { return ((key & 3) << 1) | ((key >> 2) & 1); }
+#ifndef PKV_ATTN_AHEAD
+#define PKV_ATTN_AHEAD 3   // LDS operand reads issued this many operands ahead of their MFMA
+#endif
+#ifndef PKV_ATTN_SCHED
+#define PKV_ATTN_SCHED 1   // interleave MFMA, VALU and LDS reads in the pipelined segments
+#endif
 
-// Scheduling pattern for the overlapped region (QK^T of the next tile next
-// to the probabilities of this one): per K-operand read, its two MFMAs
-// (32 cycles each) with about eight VALU instructions in their shadow.
-#ifndef PKV_ATTN_PINGPONG
-#define PKV_ATTN_PINGPONG 1
-#endif
-#ifndef PKV_ATTN_INTERLEAVE
-#define PKV_ATTN_INTERLEAVE 1
-#endif
-template <int KS>
-__device__ inline void interleave_region() {
-    if (!PKV_ATTN_INTERLEAVE) return;
-#pragma unroll
-    for (int i = 0; i < 2 * KS; ++i) {
-        if (i % 2 == 0) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                   // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);                   // VALU
-    }
+// XOR swizzles of a row's 16-byte chunk index by its key.  LDS has 64 banks
+// of 4 bytes (256 bytes per cycle); the rows one read touches must spread
+// over the 16 bank groups of 16 bytes.
+//   D = 128 (16 chunks per row, every row starting at bank 0):
+//     K tiles: an operand read takes one logical chunk from 16 consecutive
+//     keys, so the swizzle is a bijection of key & 15.
+//     V tiles: a transposed read takes a 4-chunk window from 4 consecutive
+//     keys, so bits 2..3 follow key & 3; depending on key & 7 only, it is the
+//     same for keys 8 apart, which keeps their reads one immediate apart.
+//     (Measured: K reads conflict free; V reads at the transposed-read rate.)
+//   D = 64 (8 chunks per row, rows alternating between bank halves): keys of
+//     one parity share a half, 3 bits suffice for both.
+template <int D>
+__device__ inline int swz_k(int key) {
+    if constexpr (D == 128) return ((key & 3) << 2) | ((key >> 2) & 3);
+    else return ((key & 3) << 1) | ((key >> 2) & 1);
+}
+template <int D>
+__device__ inline int swz_v(int key) {
+    if constexpr (D == 128) return (key & 3) << 2;
+    else return ((key & 3) << 1) | ((key >> 2) & 1);
 }
 
 template <int D, int QB, int NW, int NS, bool PIPE>
-__global__ __launch_bounds__(NW * 64, NW == 4 && NS == 2 ? 2 : 1) void attn_gqa_bf16_kernel(AttnArgs a, Plan p) {
+__global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, Plan p) {
     constexpr int CH = D / 8;              // 16-byte chunks per row
-    constexpr int PER = 2 * CH / NW;       // LDS-DMA loads per wave per tile (K and V)
+    constexpr int BN = PIPE ? 32 : 64;     // keys per tile
+    constexpr int NKB = BN / 32;           // 32-key blocks per tile
+    constexpr int KBLK = BN * CH / 64;     // 64-lane LDS-DMA blocks per K (or V) tile
+    constexpr int PER = 2 * KBLK / NW;     // LDS-DMA loads per wave per tile (K and V)
     constexpr int KS = D / 16;             // MFMA k-steps over channels
     constexpr int DB = D / 32;             // 32-channel output blocks
     constexpr int TE = BN * D;             // elements of one K or V tile
-    static_assert(2 * CH % NW == 0, "tile loads must split evenly over the waves");
+    static_assert(2 * KBLK % NW == 0, "tile loads must split evenly over the waves");
     static_assert(NS >= 2 && NS <= 4, "2..4 stages");
 
-    // K stages, then V stages: same-kind stages sit within 48 KB of each other,
-    // so one address register per operand serves every stage through the
-    // 16-bit immediate offset of the LDS read.
-    __shared__ __attribute__((aligned(16))) uint16_t k0[TE], k1[TE], k2[NS > 2 ? TE : 8], k3[NS > 3 ? TE : 8];
-    __shared__ __attribute__((aligned(16))) uint16_t v0[TE], v1[TE], v2[NS > 2 ? TE : 8], v3[NS > 3 ? TE : 8];
-    __shared__ int red[NW];
-    // Stage selectors; every call site passes a constant after unrolling, so
-    // each LDS access names one array and the compiler can tell in-flight
-    // LDS-DMA writes to one stage from reads of another.
-    auto kst = [&](int st) -> uint16_t* { return st == 0 ? k0 : st == 1 ? k1 : st == 2 ? k2 : k3; };
-    auto vst = [&](int st) -> uint16_t* { return st == 0 ? v0 : st == 1 ? v1 : st == 2 ? v2 : v3; };
+    // One LDS block: NS K stages, then NS V stages.  Stage offsets are
+    // compile-time constants after unrolling, so one address register per
+    // operand serves every stage through the 16-bit immediate offset of the
+    // LDS read (K stages within 48 KB of the block, V stages of the V half).
+    __shared__ __attribute__((aligned(16))) uint16_t stage_lds[2 * NS * TE];
+    __shared__ int red[NW], red_min[NW];
+    auto kst = [&](int st) -> uint16_t* __attribute__((always_inline)) { return stage_lds + st * TE; };
+    auto vst = [&](int st) -> uint16_t* __attribute__((always_inline)) { return stage_lds + (NS + st) * TE; };
 
     int group, rb;
     if (!decode(p, group, rb)) return;
@@ -113,11 +114,17 @@ __global__ __launch_bounds__(NW * 64, NW == 4 && NS == 2 ? 2 : 1) void attn_gqa_
     }
     const int wmin = wave_min_i(rmin);
     const int wmax = wave_max_i(rmax);
-    if (lane == 0) red[wave] = wmax;
+    if (lane == 0) {
+        red[wave] = wmax;
+        red_min[wave] = wmin;
+    }
     __syncthreads();
-    int e_max = 0;
+    int e_max = 0, e_min = 0x7fffffff;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) e_max = max(e_max, red[w]);
+    for (int w = 0; w < NW; ++w) {
+        e_max = max(e_max, red[w]);
+        e_min = min(e_min, red_min[w]);
+    }
 
     const int k_begin = split * p.chunk;
     const int loop_end = min(min(si.kvl, k_begin + p.chunk), e_max);
@@ -144,41 +151,68 @@ __global__ __launch_bounds__(NW * 64, NW == 4 && NS == 2 ? 2 : 1) void attn_gqa_
     const int64_t kss = a.k_stride[2], vss = a.v_stride[2];
     const int last_key = loop_end - 1;
 
-    // Per-lane source offsets (bytes, relative to the tile's first key) of the
-    // PER 16-byte chunks this lane moves per tile; lane l of block b fills LDS
-    // chunk slot b*64 + l, i.e. key slot/CH, physical chunk slot%CH, which
-    // holds logical chunk (phys ^ swz(key)) of that key's row.
-    int32_t src_off[PER];
-    int key_of[PER];
+    // LDS-DMA: every tile is KBLK 64-lane blocks of K, then KBLK of V; wave w
+    // moves blocks w*PER .. w*PER+PER-1 (all K or all V).  Lane l of block b
+    // fills LDS chunk slot b*64 + l, i.e. key slot/CH, physical chunk slot%CH,
+    // which holds logical chunk (phys ^ swizzle(key)) of that key's row.
+    static_assert(KBLK % PER == 0, "a wave's blocks must be all K or all V");
+    const bool wave_v = wave * PER >= KBLK;
+    const int blk0 = (wave * PER) % KBLK;
+    const char* const tens = (const char*)(wave_v ? vbase : kbase);
+    const int64_t trow = (wave_v ? vss : kss) * 2;   // bytes between keys
+    auto dma_key = [&](int i) __attribute__((always_inline)) { return ((blk0 + i) * 64 + lane) / CH; };
+    uint32_t src_off[PER];   // bytes from the tile's first key
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-        const int q = wave * PER + i;
-        const bool isv = q >= CH;
-        const int slot = (isv ? q - CH : q) * 64 + lane;
-        key_of[i] = slot / CH;
-        const int logical = (slot % CH) ^ swz(key_of[i]);
-        src_off[i] = (int32_t)((int64_t)key_of[i] * (isv ? vss : kss) * 2 + logical * 16);
+        const int key = dma_key(i);
+        const int logical = (lane % CH) ^ (wave_v ? swz_v<D>(key) : swz_k<D>(key));
+        src_off[i] = (uint32_t)(key * trow + logical * 16);
     }
     // Stage the tile starting at key t0.  A tile that runs past the last
     // visible key re-reads that key for the missing rows (masked later).
-    auto issue = [&](int t0, uint16_t* ks_dst, uint16_t* vs_dst) {
-        const bool full = t0 + BN <= loop_end;
-        const char* kt = (const char*)(kbase + (int64_t)t0 * kss);
-        const char* vt = (const char*)(vbase + (int64_t)t0 * vss);
+    auto issue = [&](int t0, uint16_t* ks_dst, uint16_t* vs_dst) __attribute__((always_inline)) {
+        const char* tile = tens + (int64_t)t0 * trow;
+        const uint32_t lds0 = lds_addr_of((wave_v ? vs_dst : ks_dst) + blk0 * 64 * 8);
+        if (t0 + BN <= loop_end) {
 #pragma unroll
-        for (int i = 0; i < PER; ++i) {
-            const int q = wave * PER + i;            // wave-uniform
-            const bool isv = q >= CH;
-            const int blk = isv ? q - CH : q;
-            int32_t off = src_off[i];
-            if (!full) {
-                const int over = t0 + key_of[i] - last_key;
-                if (over > 0) off -= over * (int32_t)((isv ? vss : kss) * 2);
+            for (int i = 0; i < PER; ++i) lds_dma16(lds0 + i * 1024, tile, src_off[i]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < PER; ++i) {
+                const int over = t0 + dma_key(i) - last_key;
+                lds_dma16(lds0 + i * 1024, tile, src_off[i] - (over > 0 ? (uint32_t)(over * trow) : 0u));
             }
-            const char* src = (isv ? vt : kt) + off;
-            uint16_t* dst = (isv ? vs_dst : ks_dst) + blk * 64 * 8;
-            __builtin_amdgcn_global_load_lds((const void*)src, PKV_LDS(void, dst), 16, 0, 0);
         }
+    };
+
+    // Per-lane LDS element offsets of the MFMA operands within a stage.  The
+    // K swizzle depends only on key & 15 and the V swizzle on key & 7, the same
+    // for a lane's K reads of every key block and its V reads of every 8 keys,
+    // so those strides are immediates:
+    //   K (A of S^T = K Q^T), k-step ks, key block kb: kofs[ks] + kb * 32 * D
+    //   V^T (A of O^T = V^T P^T), 16-key step st, half b, channel block db:
+    //       vofs[db] + (st * 16 + b * 8) * D
+    int kofs[KS], vofs[DB];
+    {
+        const int sk = swz_k<D>(j);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) kofs[ks] = j * D + (((ks * 2 + hl) ^ sk) << 3);
+        const int g = lane >> 4, sl = lane & 15;
+        const int vkey = (g >> 1) * 4 + (sl >> 2);   // key within its group of 8
+        const int sv = swz_v<D>(vkey);
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+            vofs[db] = vkey * D + (((db * 4 + (g & 1) * 2 + ((sl & 3) >> 1)) ^ sv) << 3) + (sl & 1) * 4;
+    }
+    auto k_operand = [&](const uint16_t* ks_src, int ks, int kb) __attribute__((always_inline)) {
+        return __builtin_bit_cast(bf16x8, *(const u32x4*)(ks_src + kofs[ks] + kb * 32 * D));
+    };
+    auto v_operand = [&](const uint16_t* vs_src, int st, int db) __attribute__((always_inline)) {
+        const uint16_t* base = vs_src + vofs[db] + st * 16 * D;
+        const s16x4 p0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(PKV_LDS(s16x4, base));
+        const s16x4 p1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(PKV_LDS(s16x4, base + 8 * D));
+        return __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){p0[0], p0[1], p0[2], p0[3],
+                                                                                       p1[0], p1[1], p1[2], p1[3]});
     };
 
     f32x16 o[DB][QB];
@@ -195,26 +229,23 @@ __global__ __launch_bounds__(NW * 64, NW == 4 && NS == 2 ? 2 : 1) void attn_gqa_
     const float sc2 = a.scale * kLog2e;
 
     // Raw scores S^T = K Q^T of the tile held in K stage ks_src.
-    auto qk = [&](const uint16_t* ks_src, f32x16 (&s)[2][QB]) {
+    auto qk = [&](const uint16_t* ks_src, f32x16 (&s)[NKB][QB]) __attribute__((always_inline)) {
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
             for (int qb = 0; qb < QB; ++qb) s[kb][qb] = f32x16{};
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                const int key = kb * 32 + j;
-                const int phys = (ks * 2 + hl) ^ swz(key);
-                const u32x4 kv = *(const u32x4*)(ks_src + key * D + phys * 8);
-                const bf16x8 kf = __builtin_bit_cast(bf16x8, kv);
+            for (int kb = 0; kb < NKB; ++kb) {
+                const bf16x8 kf = k_operand(ks_src, ks, kb);
 #pragma unroll
                 for (int qb = 0; qb < QB; ++qb)
                     s[kb][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][ks], s[kb][qb], 0, 0, 0);
             }
         }
         // Keep the K-operand reads one or two MFMAs ahead instead of all at once.
-        sched_reads_mfma<2 * KS, 1, QB>();
+        sched_reads_mfma<NKB * KS, 1, QB>();
     };
 
     // Softmax, part 1 (branchy, before the overlapped region): mask the raw
@@ -224,13 +255,13 @@ __global__ __launch_bounds__(NW * 64, NW == 4 && NS == 2 ? 2 : 1) void attn_gqa_
     // rescaling O; probabilities then stay below 2^kLazy, well inside fp32 and
     // bf16 range, and the final O/l is unchanged.
     constexpr float kLazy = 8.0f;
-    auto row_max = [&](int t0, f32x16 (&s)[2][QB], auto mask_tag) {
+    auto row_max = [&](int t0, f32x16 (&s)[NKB][QB], auto mask_tag) __attribute__((always_inline)) {
         constexpr bool MASK = decltype(mask_tag)::value;
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
             if (MASK) {
 #pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
+                for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
                     for (int r = 0; r < 16; ++r) {
                         const int key = t0 + kb * 32 + (r >> 2) * 8 + hl * 4 + (r & 3);
@@ -241,14 +272,14 @@ __global__ __launch_bounds__(NW * 64, NW == 4 && NS == 2 ? 2 : 1) void attn_gqa_
             if (sc2 >= 0.f) {
                 mx = -INFINITY;
 #pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
+                for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
                     for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][qb][r]);
                 mx = fmaxf(mx, __shfl_xor(mx, 32));
             } else {
                 mx = INFINITY;
 #pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
+                for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
                     for (int r = 0; r < 16; ++r) mx = fminf(mx, s[kb][qb][r]);
                 mx = fminf(mx, __shfl_xor(mx, 32));
@@ -269,14 +300,14 @@ __global__ __launch_bounds__(NW * 64, NW == 4 && NS == 2 ? 2 : 1) void attn_gqa_
     // Softmax, part 2 (branch-free): probabilities, row sums and the bf16
     // P^T operands.  Masked scores are +-inf here; their probability is
     // forced to 0 (also when the scale is 0).
-    auto probs = [&](int t0, f32x16 (&s)[2][QB], bf16x8 (&pb)[QB][4], auto mask_tag) {
+    auto probs = [&](int t0, f32x16 (&s)[NKB][QB], bf16x8 (&pb)[QB][2 * NKB], auto mask_tag) __attribute__((always_inline)) {
         constexpr bool MASK = decltype(mask_tag)::value;
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
             const float neg_m = m_run[qb] == -INFINITY ? 0.f : -m_run[qb];
             float lsum = 0.f;
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
+            for (int kb = 0; kb < NKB; ++kb) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     float e = __builtin_amdgcn_exp2f(fmaf(s[kb][qb][r], sc2, neg_m));
@@ -290,7 +321,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 && NS == 2 ? 2 : 1) void attn_gqa_
             }
             l_run[qb] += lsum;
 #pragma unroll
-            for (int st = 0; st < 4; ++st) {
+            for (int st = 0; st < 2 * NKB; ++st) {
                 f32x8 pv;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) pv[e] = s[st >> 1][qb][(st & 1) * 8 + e];
@@ -300,138 +331,303 @@ __global__ __launch_bounds__(NW * 64, NW == 4 && NS == 2 ? 2 : 1) void attn_gqa_
     };
 
     // O^T += V^T P^T for the tile held in V stage vs_src.
-    auto pv = [&](const uint16_t* vs_src, const bf16x8 (&pb)[QB][4]) {
-        // O^T += V^T P^T.  Lane group g (16 lanes) reads channels
-        // 32db + 16(g&1) .. +15 for keys {16st + 8b + 4(g>>1) + 0..3}, b = 0, 1.
-        const int g = lane >> 4, sl = lane & 15;
-        const int hh = g >> 1;
+    auto pv = [&](const uint16_t* vs_src, const bf16x8 (&pb)[QB][2 * NKB]) __attribute__((always_inline)) {
+        // Lane group g (16 lanes) reads channels 32db + 16(g&1) .. +15 for
+        // keys {16st + 8b + 4(g>>1) + 0..3}, b = 0, 1: the key order of the
+        // P^T accumulator rows.
 #pragma unroll
-        for (int st = 0; st < 4; ++st) {
+        for (int st = 0; st < 2 * NKB; ++st) {
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
-                s16x4 part[2];
-#pragma unroll
-                for (int b = 0; b < 2; ++b) {
-                    const int key = st * 16 + b * 8 + hh * 4 + (sl >> 2);
-                    const int col = db * 32 + (g & 1) * 16 + (sl & 3) * 4;
-                    const int phys = (col >> 3) ^ swz(key);
-                    const uint16_t* ptr = vs_src + key * D + phys * 8 + (col & 7);
-                    part[b] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(PKV_LDS(s16x4, ptr));
-                }
-                const s16x4 p0 = part[0], p1 = part[1];
-                const bf16x8 vf = __builtin_bit_cast(
-                    bf16x8, (short __attribute__((ext_vector_type(8)))){p0[0], p0[1], p0[2], p0[3], p1[0], p1[1],
-                                                                          p1[2], p1[3]});
+                const bf16x8 vf = v_operand(vs_src, st, db);
 #pragma unroll
                 for (int qb = 0; qb < QB; ++qb)
                     o[db][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[qb][st], o[db][qb], 0, 0, 0);
             }
         }
-        sched_reads_mfma<4 * DB, 2, QB>();
+        sched_reads_mfma<2 * NKB * DB, 2, QB>();
     };
 
-    // Software pipeline over key tiles.  Stage i % NS holds tile i; tile i is
-    // issued NS-1 iterations ahead.  Iteration i runs QK^T of tile i+1 (MFMA)
-    // next to the softmax of tile i (VALU), then PV of tile i, so the two
-    // units overlap within a wave.  Tile i's K is read in iteration i-1 and its
-    // V in iteration i; the barrier closing iteration i-1 frees its stage for
-    // tile i+NS-1 and publishes tile i+1 (waited for by every wave before it).
-    static_assert(!PIPE || NS == 4, "the ping-pong schedule uses four LDS stages");
-    auto wait_outstanding = [&](int tiles_after) {
+    // Tiles are staged through NS LDS stages: tile i lives in stage i % NS
+    // and is issued NS-1 tiles ahead of its use.
+    auto wait_outstanding = [&](int tiles_after) __attribute__((always_inline)) {
         if (NS > 3 && tiles_after >= 3) wait_vmcnt<(NS > 3 ? 3 : 1) * PER>();
         else if (NS > 2 && tiles_after >= 2) wait_vmcnt<(NS > 2 ? 2 : 1) * PER>();
         else if (tiles_after == 1) wait_vmcnt<PER>();
         else wait_vmcnt<0>();
     };
+    auto lds_reads_done = []() __attribute__((always_inline)) { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14)); };
+
+    // One tile in plain order: wait for it, then QK^T, softmax and PV back to
+    // back.  The barrier that publishes tile i also proves every wave finished
+    // tile i-1, so tile i-1's stage is refilled with tile i+NS-1 right after.
+    auto plain_tile = [&](int i, auto stage_tag) __attribute__((always_inline)) {
+        constexpr int S = decltype(stage_tag)::value;
+        wait_outstanding(min(i + NS - 2, n_tiles - 1) - i);
+        lds_reads_done();
+        bare_barrier();
+        const int ahead = i + NS - 1;
+        if (ahead < n_tiles) issue(k_begin + ahead * BN, kst((S + NS - 1) % NS), vst((S + NS - 1) % NS));
+        f32x16 sc[NKB][QB];
+        qk(kst(S), sc);
+        bf16x8 pb[QB][2 * NKB];
+        const int t0 = k_begin + i * BN;
+        if (t0 + BN > wmin) {
+            row_max(t0, sc, std::true_type{});
+            probs(t0, sc, pb, std::true_type{});
+        } else {
+            row_max(t0, sc, std::false_type{});
+            probs(t0, sc, pb, std::false_type{});
+        }
+        pv(vst(S), pb);
+    };
+    auto plain_from = [&](int first) __attribute__((always_inline)) {
+        for (int t = first & ~(NS - 1); t < n_tiles; t += NS) {
+            static_for<0, NS>([&](auto s_tag) {
+                const int i = t + decltype(s_tag)::value;
+                if (i >= first && i < n_tiles) plain_tile(i, s_tag);
+            });
+        }
+    };
+
 #pragma unroll
-    for (int s = 0; s < (PIPE ? 1 : NS - 1); ++s)
+    for (int s = 0; s < NS - 1; ++s)
         if (s < n_tiles) issue(k_begin + s * BN, kst(s), vst(s));
+
     if constexpr (!PIPE) {
-        // Plain order: tile i is waited for, then QK^T, softmax and PV run back
-        // to back.  The barrier that publishes tile i also proves every wave
-        // finished tile i-1, so tile i-1's stage is refilled right after it.
-        for (int t = 0; t < n_tiles; t += NS) {
-#pragma unroll
-            for (int s = 0; s < NS; ++s) {
-                const int i = t + s;
-                if (i < n_tiles) {
-                    wait_outstanding(min(i + NS - 2, n_tiles - 1) - i);
-                    __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
-                    bare_barrier();
-                    const int ahead = i + NS - 1;
-                    if (ahead < n_tiles)
-                        issue(k_begin + ahead * BN, kst((s + NS - 1) % NS), vst((s + NS - 1) % NS));
-                    f32x16 sc[2][QB];
-                    qk(kst(s), sc);
-                    bf16x8 pb[QB][4];
-                    const int t0 = k_begin + i * BN;
-                    if (t0 + BN > wmin) {
-                        row_max(t0, sc, std::true_type{});
-                        probs(t0, sc, pb, std::true_type{});
-                    } else {
-                        row_max(t0, sc, std::false_type{});
-                        probs(t0, sc, pb, std::false_type{});
-                    }
-                    pv(vst(s), pb);
-                }
-            }
-        }
+        plain_from(0);
     } else {
-        // Ping-pong schedule.  The 8 waves form two groups of 4 (waves w and
-        // w+4 share a SIMD); group 1 runs one half-step behind group 0.  A wave
-        // alternates an MFMA phase (PV of its previous tile, then QK^T of its
-        // next tile) with a VALU phase (softmax of that tile), so at every
-        // half-step each SIMD holds one wave in each phase and the matrix core
-        // and the VALU work at the same time.  Tile t is read in half-steps
-        // 2t .. 2t+3; it is issued at half-step 2t-4 into the stage that tile
-        // t-4 left, and every wave waits for it before the barrier that opens
-        // half-step 2t.
-        static_assert(NW == 8, "two groups of four waves");
-        const int gp = wave >> 2;
-        f32x16 sc[2][QB];
-        bf16x8 pb[QB][4];
-        auto mfma_phase = [&](int t, const uint16_t* vs_prev, const uint16_t* ks_cur) {
-            if (t >= 1 && t - 1 < n_tiles) pv(vs_prev, pb);
-            if (t < n_tiles) qk(ks_cur, sc);
-        };
-        auto valu_phase = [&](int t) {
-            if (t < 0 || t >= n_tiles) return;
-            const int t0 = k_begin + t * BN;
-            if (t0 + BN > wmin) {
-                row_max(t0, sc, std::true_type{});
-                probs(t0, sc, pb, std::true_type{});
-            } else {
-                row_max(t0, sc, std::false_type{});
-                probs(t0, sc, pb, std::false_type{});
+        // Intra-wave software pipeline over the leading tiles that need no
+        // mask (F of them, the same for every wave); tiles are 32 keys (one
+        // key block).  With S(t) the raw scores of tile t, iteration t runs
+        //   segment 1: S(t+1) = K Q^T (MFMA) interleaved with the
+        //              probabilities of tile t (exp2, VALU);
+        //   segment 2: O += V^T P(t) (MFMA) interleaved with the row maxima of
+        //              S(t+1) and the row sums of P(t) (VALU);
+        // then moves the reference maximum if needed.  A wave that alternates
+        // its own MFMA and VALU instructions keeps both units busy; an
+        // MFMA-only and a VALU-only wave sharing a SIMD overlap far less.  Two
+        // workgroups of four waves share each CU, so the two waves on a SIMD
+        // never wait at each other's barriers.  Iteration t reads K of tile
+        // t+1 and V of tile t; tile t+3 is issued after the barrier opening
+        // it, into the stage that tile t-1 left.
+        static_assert(NS == 4 && NKB == 1, "the pipelined schedule uses four LDS stages of 32-key tiles");
+        const int F = sc2 > 0.f ? max(0, min(n_tiles, (e_min - k_begin) / BN)) : 0;
+        const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+
+        // Segment 1: nxt = raw scores of key block kbn of the K stage; the
+        // probabilities of cur into pb (two 16-key operands per row block).
+        // Written as fenced groups of one K operand's MFMAs, their share of
+        // the VALU work and the operand read PKV_ATTN_AHEAD steps ahead, so
+        // the LDS reads stay in flight across MFMAs.
+        auto seg1 = [&](const uint16_t* ks_src, int kbn, f32x16 (&cur)[QB], f32x16 (&nxt)[QB],
+                        bf16x8 (&pb)[QB][2]) __attribute__((always_inline)) {
+            constexpr int A = PKV_ATTN_AHEAD < KS ? PKV_ATTN_AHEAD : KS;
+            constexpr int PER_K = 16 / KS;   // probabilities per k-step and row block
+            bf16x8 kop[KS];
+#pragma unroll
+            for (int q = 0; q < A; ++q) kop[q] = k_operand(ks_src, q, kbn);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int q = 0; q < KS; ++q) {
+#pragma unroll
+                for (int qb = 0; qb < QB; ++qb) {
+                    nxt[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[q], qf[qb][q], q == 0 ? f32x16{} : nxt[qb],
+                                                                     0, 0, 0);
+                    const float neg_m = -m_run[qb];
+#pragma unroll
+                    for (int r = q * PER_K; r < (q + 1) * PER_K; ++r)
+                        cur[qb][r] = __builtin_amdgcn_exp2f(fmaf(cur[qb][r], sc2, neg_m));
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        if ((q + 1) * PER_K == 8 * (h + 1)) {
+                            f32x8 pv8;
+#pragma unroll
+                            for (int e = 0; e < 8; ++e) pv8[e] = cur[qb][h * 8 + e];
+                            pb[qb][h] = __builtin_convertvector(pv8, bf16x8);
+                        }
+                    }
+                }
+                if (q + A < KS) kop[q + A] = k_operand(ks_src, q + A, kbn);
+                __builtin_amdgcn_sched_barrier(0);
             }
         };
-        if (n_tiles > 1) issue(k_begin + BN, kst(1), vst(1));   // tile 0 went out above
-        if (n_tiles > 0) {
-            wait_outstanding(n_tiles > 1 ? 1 : 0);
-            bare_barrier();
-        }
-        const int H = 2 * n_tiles + 2;
-        for (int h0 = 0; h0 < H; h0 += 8) {
+
+        // Segment 2: O^T += V^T P^T for key block kbc of the V stage; the row
+        // maxima of nxt (over both lanes of a row, into mx) and the row sums
+        // of pb alongside, in fenced groups as in segment 1.
+        auto seg2 = [&](const uint16_t* vs_src, int kbc, const bf16x8 (&pb)[QB][2], const f32x16 (&nxt)[QB],
+                        float (&mx)[QB]) __attribute__((always_inline)) {
+            constexpr int NQ = 2 * DB;                 // V operands: two 16-key steps x DB channel blocks
+            constexpr int A = PKV_ATTN_AHEAD < NQ ? PKV_ATTN_AHEAD : NQ;
+            constexpr int PER_M = 16 / NQ;             // maxima per operand and row block
+            constexpr int PER_D = 8 / NQ > 0 ? 8 / NQ : 1;   // sum steps per operand and row block
+            bf16x8 vop[NQ];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int h = h0 + e;
-                if (h < H) {
-                    const int m = h >> 1;
-                    const int sm = e >> 1;   // == m % 4
-                    if ((e & 1) == 0) {
-                        if (m + 2 < n_tiles) issue(k_begin + (m + 2) * BN, kst((sm + 2) % 4), vst((sm + 2) % 4));
-                        if (gp == 0) mfma_phase(m, vst((sm + 3) % 4), kst(sm));
-                        else valu_phase(m - 1);
-                    } else {
-                        if (gp == 0) valu_phase(m);
-                        else mfma_phase(m, vst((sm + 3) % 4), kst(sm));
-                        if (m + 1 < n_tiles) wait_outstanding(min(m + 2, n_tiles - 1) - (m + 1));
+            for (int q = 0; q < A; ++q) vop[q] = v_operand(vs_src, 2 * kbc + q / DB, q % DB);
+            __builtin_amdgcn_sched_barrier(0);
+            float m0[QB], m1[QB], l0[QB], l1[QB];
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) {
+                m0[qb] = -INFINITY;
+                m1[qb] = -INFINITY;
+                l0[qb] = 0.f;
+                l1[qb] = 0.f;
+            }
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) {
+                const int h = q / DB, db = q % DB;
+#pragma unroll
+                for (int qb = 0; qb < QB; ++qb) {
+                    o[db][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[q], pb[qb][h], o[db][qb], 0, 0, 0);
+#pragma unroll
+                    for (int r = q * PER_M; r < (q + 1) * PER_M; r += 2) {
+                        m0[qb] = fmaxf(m0[qb], nxt[qb][r]);
+                        m1[qb] = fmaxf(m1[qb], nxt[qb][r + 1]);
                     }
-                    __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
-                    bare_barrier();
+#pragma unroll
+                    for (int d = q * PER_D; d < (q + 1) * PER_D && d < 8; ++d) {
+                        const bf16x8 pp = pb[qb][d >> 2];
+                        const int e = (d & 3) * 2;
+                        if (d & 1) l1[qb] = __builtin_amdgcn_fdot2_f32_bf16((bf16x2){pp[e], pp[e + 1]}, ones, l1[qb], false);
+                        else l0[qb] = __builtin_amdgcn_fdot2_f32_bf16((bf16x2){pp[e], pp[e + 1]}, ones, l0[qb], false);
+                    }
+                }
+                if (q + A < NQ) vop[q + A] = v_operand(vs_src, 2 * kbc + (q + A) / DB, (q + A) % DB);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) {
+                l_run[qb] += l0[qb] + l1[qb];
+                // lanes l and l+32 hold the two 16-key halves of the same row
+                const float m = fmaxf(m0[qb], m1[qb]);
+                const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+                mx[qb] = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+            }
+        };
+
+        // Move the reference maxima after the tile's PV (lazily, as row_max).
+        auto move_max = [&](const float (&mx)[QB]) __attribute__((always_inline)) {
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) {
+                const float msc = mx[qb] * sc2;
+                const bool up = msc > m_run[qb] + kLazy;
+                if (__builtin_amdgcn_ballot_w64(up) != 0) {
+                    const float m_new = up ? msc : m_run[qb];
+                    const float alpha = m_run[qb] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[qb] - m_new);
+                    l_run[qb] *= alpha;
+#pragma unroll
+                    for (int db = 0; db < DB; ++db) o[db][qb] *= alpha;
+                    m_run[qb] = m_new;
                 }
             }
+        };
+
+        // One step: scores of the next tile from ks_next, the current tile's
+        // probabilities and PV from vs_cur.
+        auto half_step = [&](const uint16_t* ks_next, int kbn, const uint16_t* vs_cur, int kbc, f32x16 (&cur)[QB],
+                             f32x16 (&nxt)[QB]) __attribute__((always_inline)) {
+            bf16x8 pb[QB][2];
+            float mx[QB];
+            seg1(ks_next, kbn, cur, nxt, pb);
+            seg2(vs_cur, kbc, pb, nxt, mx);
+            move_max(mx);
+        };
+
+        auto iteration = [&](int i, auto u_tag, f32x16 (&cur)[QB], f32x16 (&nxt)[QB]) __attribute__((always_inline)) {
+            constexpr int U = decltype(u_tag)::value;
+            if (i + 2 < n_tiles) wait_vmcnt<PER>();
+            else wait_vmcnt<0>();
+            lds_reads_done();
+            bare_barrier();
+            if (i + 3 < n_tiles) issue(k_begin + (i + 3) * BN, kst((U + 3) % NS), vst((U + 3) % NS));
+            half_step(kst((U + 1) % NS), 0, vst(U), 0, cur, nxt);
+        };
+
+        // Last pipelined tile: probabilities and PV without overlap; issues
+        // the tile that plain order would issue at this point.
+        auto drain = [&](int i, auto u_tag, f32x16 (&cur)[QB]) __attribute__((always_inline)) {
+            constexpr int U = decltype(u_tag)::value;
+            lds_reads_done();
+            bare_barrier();
+            if (i + 3 < n_tiles) issue(k_begin + (i + 3) * BN, kst((U + 3) % NS), vst((U + 3) % NS));
+            bf16x8 pb[QB][2];
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) {
+                const float neg_m = -m_run[qb];
+                float lsum = 0.f;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    cur[qb][r] = __builtin_amdgcn_exp2f(fmaf(cur[qb][r], sc2, neg_m));
+                    lsum += cur[qb][r];
+                }
+                l_run[qb] += lsum;
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    f32x8 pv8;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) pv8[e] = cur[qb][h * 8 + e];
+                    pb[qb][h] = __builtin_convertvector(pv8, bf16x8);
+                }
+            }
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    const bf16x8 vf = v_operand(vst(U), h, db);
+#pragma unroll
+                    for (int qb = 0; qb < QB; ++qb)
+                        o[db][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[qb][h], o[db][qb], 0, 0, 0);
+                }
+        };
+
+        if (F >= 2) {
+            f32x16 sA[QB], sB[QB];
+            wait_outstanding(min(NS - 2, n_tiles - 1));
+            lds_reads_done();
+            bare_barrier();
+            // scores of tile 0 and their maxima
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) sA[qb] = f32x16{};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                const bf16x8 kf = k_operand(kst(0), ks, 0);
+#pragma unroll
+                for (int qb = 0; qb < QB; ++qb)
+                    sA[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][ks], sA[qb], 0, 0, 0);
+            }
+            {
+                float mx[QB];
+#pragma unroll
+                for (int qb = 0; qb < QB; ++qb) {
+                    float m = sA[qb][0];
+#pragma unroll
+                    for (int r = 1; r < 16; ++r) m = fmaxf(m, sA[qb][r]);
+                    const auto sw =
+                        __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+                    mx[qb] = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+                }
+                move_max(mx);
+            }
+            for (int t = 0; t + 1 < F; t += NS) {
+                static_for<0, NS>([&](auto u_tag) {
+                    constexpr int u = decltype(u_tag)::value;
+                    const int i = t + u;
+                    if (i + 1 < F) {
+                        if constexpr (u % 2 == 0) iteration(i, u_tag, sA, sB);
+                        else iteration(i, u_tag, sB, sA);
+                    }
+                });
+            }
+            const int last = F - 1;
+            switch (last & 3) {
+                case 0: drain(last, std::integral_constant<int, 0>{}, sA); break;
+                case 1: drain(last, std::integral_constant<int, 1>{}, sB); break;
+                case 2: drain(last, std::integral_constant<int, 2>{}, sA); break;
+                default: drain(last, std::integral_constant<int, 3>{}, sB); break;
+            }
         }
+        plain_from(F >= 2 ? F : 0);
     }
 
     // Finish each row: the two lanes of a column hold disjoint partial sums.
@@ -475,23 +671,19 @@ __global__ __launch_bounds__(NW * 64, NW == 4 && NS == 2 ? 2 : 1) void attn_gqa_
     }
 }
 
-template <int D, int QB, int NW>
-hipError_t launch_shape(const AttnArgs& a, const Plan& p, dim3 grid, hipStream_t stream) {
-    if constexpr (NW == 8) {   // two wave groups per SIMD: ping-pong schedule
-        hipLaunchKernelGGL((attn_gqa_bf16_kernel<D, QB, NW, 4, PKV_ATTN_PINGPONG != 0>), grid, dim3(NW * 64), 0,
-                           stream, a, p);
-    } else if (p.ns == 2) {    // two independent workgroups per CU
-        hipLaunchKernelGGL((attn_gqa_bf16_kernel<D, QB, NW, 2, false>), grid, dim3(NW * 64), 0, stream, a, p);
-    } else {
-        hipLaunchKernelGGL((attn_gqa_bf16_kernel<D, QB, NW, 3, false>), grid, dim3(NW * 64), 0, stream, a, p);
-    }
-    return hipGetLastError();
-}
-
+// Kernel shapes (Plan.ns): 4 waves x 32 rows, two workgroups per CU, and
+//   ns == 4: 32-key tiles, software-pipelined (64 KB of LDS stages);
+//   ns == 2: 64-key tiles, plain order (64 KB of LDS stages).
 template <int D>
 hipError_t launch_d(const AttnArgs& a, const Plan& p, dim3 grid, hipStream_t stream) {
-    if (p.nw == 8) return launch_shape<D, 1, 8>(a, p, grid, stream);
-    return launch_shape<D, 1, 4>(a, p, grid, stream);
+    if (p.nw != 4 || p.qb != 1) return hipErrorInvalidValue;
+    if (p.ns == 4)
+        hipLaunchKernelGGL((attn_gqa_bf16_kernel<D, 1, 4, 4, true>), grid, dim3(256), 0, stream, a, p);
+    else if (p.ns == 2)
+        hipLaunchKernelGGL((attn_gqa_bf16_kernel<D, 1, 4, 2, false>), grid, dim3(256), 0, stream, a, p);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
 }
 
 }  // namespace

@@ -112,17 +112,17 @@ __global__ __launch_bounds__(256) void attn_mla_bf16_kernel(AttnArgs a, Plan p) 
         src_off[i] = (int32_t)((int64_t)key_of[i] * kss * 2 + logical * 16);
     }
     auto issue = [&](int t0, uint16_t* dst_stage) {
-        const bool full = t0 + MBN <= loop_end;
         const char* kt = (const char*)(kbase + (int64_t)t0 * kss);
+        const uint32_t lds0 = lds_addr_of(dst_stage + wave * PER * 64 * 8);
+        if (t0 + MBN <= loop_end) {
 #pragma unroll
-        for (int i = 0; i < PER; ++i) {
-            int32_t off = src_off[i];
-            if (!full) {
+            for (int i = 0; i < PER; ++i) lds_dma16(lds0 + i * 1024, kt, (uint32_t)src_off[i]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < PER; ++i) {
                 const int over = t0 + key_of[i] - last_key;
-                if (over > 0) off -= over * (int32_t)(kss * 2);
+                lds_dma16(lds0 + i * 1024, kt, (uint32_t)(src_off[i] - (over > 0 ? over * (int32_t)(kss * 2) : 0)));
             }
-            uint16_t* dst = dst_stage + (wave * PER + i) * 64 * 8;
-            __builtin_amdgcn_global_load_lds((const void*)(kt + off), PKV_LDS(void, dst), 16, 0, 0);
         }
     };
 
