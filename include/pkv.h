@@ -77,8 +77,9 @@ enum { PKV_ATTN_GQA = 0, PKV_ATTN_MLA = 1 };
  * Geometry this build implements (else PKV_ERR_UNSUPPORTED), with
  * E = 16 / element size (8 for bf16, 4 for fp32):
  *   head_dim, v_dim, rope_offset multiples of E; head_dim and v_dim multiples
- *   of 2E; rope_dim a multiple of 2E.  This covers d = 64/128 GQA heads and
- *   the 576-channel MLA row [c_kv (512) | k_pe (64)] with rope_offset 512. */
+ *   of 2E; rope_dim a multiple of 2E and at most 256.  This covers d = 64/128
+ *   (and 256) GQA heads and the 576-channel MLA row [c_kv (512) | k_pe (64)]
+ *   with rope_offset 512. */
 typedef struct pkv_layout {
     int32_t dtype;          /* PKV_BF16 or PKV_F32 */
     int32_t n_layers;
@@ -105,9 +106,10 @@ typedef struct pkv_layout {
  *     dst_k[l][h][dst_pos[t]] = R(delta_t) src_k[l][h][t]   (rotary slice; other channels bit-exact)
  *     dst_v[l][h][dst_pos[t]] = src_v[l][h][t]              (bit-exact)
  * src_pos / dst_pos: device int32 [n_tokens], any sign, |delta| < 2^24.
- * Rotation arithmetic: the angle delta*omega_i and its cos/sin are formed in
- * fp64, rounded to fp32, and the rotation runs in fp32 with one
- * round-to-nearest-even to the storage type.  delta_t == 0 copies the row
+ * Rotation arithmetic: omega_i is computed on the host in fp64; the angle
+ * delta*omega_i is formed and reduced modulo pi/2 in fp64, its cos/sin are
+ * evaluated in fp32 (absolute error below 1e-7), and the rotation runs in fp32
+ * with one round-to-nearest-even to the storage type.  delta_t == 0 copies the row
  * bit-exact.  Destination slots other than dst_pos[] are not touched.  A token
  * with dst_pos outside [0, dst_capacity) is skipped (and *err_flag set).
  * In-place use (dst_k == src_k with identical strides, same for V) is allowed
@@ -116,7 +118,8 @@ typedef struct pkv_layout {
  * Errors: PKV_ERR_NULL (layout, src_k, dst_k, src_pos, dst_pos; src_v/dst_v
  * when v_dim > 0), PKV_ERR_SHAPE (non-positive sizes, rope_dim odd or <= 0,
  * rope slice outside the row, n_tokens < 0, theta <= 0), PKV_ERR_ALIGN,
- * PKV_ERR_ALIAS, PKV_ERR_UNSUPPORTED, PKV_ERR_DEVICE. */
+ * PKV_ERR_ALIAS, PKV_ERR_UNSUPPORTED (dtype, style, row geometry, rope_dim >
+ * 256), PKV_ERR_DEVICE. */
 pkv_status pkv_reposition_splice(const void* src_k, const void* src_v, void* dst_k, void* dst_v,
                                  const int32_t* src_pos, const int32_t* dst_pos, float rope_theta,
                                  int32_t rope_dim, const pkv_layout* layout, void* stream);

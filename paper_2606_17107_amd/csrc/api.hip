@@ -79,6 +79,9 @@ pkv_status check_splice(const void* src_k, const void* src_v, void* dst_k, void*
                     L->n_layers, L->n_kv_heads, L->head_dim, L->v_dim, L->n_tokens, L->dst_capacity);
     if (rope_dim <= 0 || (rope_dim & 1))
         return fail(PKV_ERR_SHAPE, "rope_dim %d must be positive and even", rope_dim);
+    if (rope_dim > 256)
+        return fail(PKV_ERR_UNSUPPORTED, "rope_dim %d: rotary slices of at most 256 channels are supported",
+                    rope_dim);
     if (L->rope_offset < 0 || (int64_t)L->rope_offset + rope_dim > L->head_dim)
         return fail(PKV_ERR_SHAPE, "rotary slice [%d, %d) lies outside the %d-channel row",
                     L->rope_offset, L->rope_offset + rope_dim, L->head_dim);

@@ -9,7 +9,9 @@
 //   * A row of K (head_dim channels) or V (v_dim channels) is cut into 16-byte
 //     chunks.  Every thread ("lane") owns two chunks of one token's row and
 //     keeps that assignment for every (layer, kv_head) row it visits, so the
-//     cos/sin of its pairs are formed once and reused from registers.
+//     cos/sin of its pairs are formed once and reused from registers.  When
+//     the whole wave shares one delta, each lane forms one pair's cos/sin and
+//     the rotary lanes gather theirs by shuffle.
 //       - rotary lane l:     chunks rope_c0+l and rope_c0+rope_nc/2+l.  With
 //         HALF pairing these hold the two partners of the same 8 (bf16) or
 //         4 (fp32) pairs; with INTERLEAVED pairing each chunk holds whole
@@ -19,12 +21,19 @@
 //     Lanes of consecutive tokens are consecutive threads, so each load or
 //     store instruction of a wave covers whole 128-byte lines of
 //     token-contiguous caches.
-//   * The angle delta*omega_i and its cos/sin are computed in fp64 once per
-//     thread and rounded to fp32; the rotation itself is fp32 with one
-//     round-to-nearest-even to bf16.  delta == 0 copies bit-exact.
-//   * The block grid is (token tiles, row chunks[, segments]); every thread
-//     walks rows_per_block (layer, kv_head) rows, issuing the loads of
-//     kUnroll rows before using them to keep bytes in flight.
+//   * omega_i = theta^(-2i/r) is tabulated on the host in fp64 and passed in
+//     the kernel arguments.  Each thread forms delta*omega_i in fp64, reduces
+//     it by pi/2 in fp64 (a two-part pi/2, so the reduced angle is accurate to
+//     ~1e-16 for any |delta| < 2^31), and evaluates sin and cos of the reduced
+//     angle in [-pi/4, pi/4] with their Taylor series in fp32 (truncation error
+//     below 2e-9).  The rotation itself is fp32 with one round-to-nearest-even
+//     to bf16.  delta == 0 copies bit-exact.
+//   * A block covers a tile of tokens and a few (layer, kv_head) rows: many
+//     small blocks keep the rows in flight at any moment close together in
+//     memory.  The grid is (token tiles, row groups, segments); token tiles are
+//     renumbered so that each XCD streams one contiguous range.  The K/V loads
+//     of the first rows are issued before the positions are read and the
+//     coefficients formed.
 #include <math.h>
 
 #include "pkv_internal.h"
@@ -36,19 +45,23 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // Launch-shape constants (tuned on MI355X; overridable at build time).
 #ifndef PKV_SPLICE_UNROLL
-#define PKV_SPLICE_UNROLL 4        // rows whose loads are issued before any is used
+#define PKV_SPLICE_UNROLL 1        // rows whose loads are issued before any is used
 #endif
-#ifndef PKV_SPLICE_TARGET_BLOCKS
-#define PKV_SPLICE_TARGET_BLOCKS 8192
+#ifndef PKV_SPLICE_ROWS
+#define PKV_SPLICE_ROWS 1          // (layer, kv_head) rows per block
 #endif
-#ifndef PKV_SPLICE_MIN_ROWS
-#define PKV_SPLICE_MIN_ROWS 8      // rows per thread at least (amortises the cos/sin)
+#ifndef PKV_SPLICE_BLOCK
+#define PKV_SPLICE_BLOCK 256       // threads per block
 #endif
 #ifndef PKV_SPLICE_NONTEMPORAL
 #define PKV_SPLICE_NONTEMPORAL 1   // streaming loads/stores: the data is touched once
 #endif
 constexpr int kUnroll = PKV_SPLICE_UNROLL;
+constexpr int kRowsPerBlock = PKV_SPLICE_ROWS;
+constexpr int kBlock = PKV_SPLICE_BLOCK;
 constexpr int kHalf = 0;
+constexpr int kWave = 64;
+constexpr int kXcds = 8;
 
 __device__ inline u32x4 ld16(const char* p) {
 #if PKV_SPLICE_NONTEMPORAL
@@ -67,7 +80,9 @@ __device__ inline void st16(char* p, u32x4 v) {
 
 struct Geo {
     int lanes_k, lanes_v, lanes, tok_per_block, rows_per_block;
-    int rope_c0, rope_nc, n_kc, n_vc, n_rows;
+    int rope_c0, rope_nc, n_kc, n_vc, n_rows, n_pairs;
+    int xcd_tiles;          // tiles per XCD when the tile count divides by 8, else 0
+    uint32_t lanes_magic;   // ceil(2^32 / lanes)
 };
 
 __device__ inline float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
@@ -80,6 +95,42 @@ __device__ inline uint32_t bf_rne(float f) {
     return u >> 16;
 }
 __device__ inline uint32_t bf_pack(float lo, float hi) { return bf_rne(lo) | (bf_rne(hi) << 16); }
+
+// Frequencies omega_i = theta^(-2i/r), fp64, for the pairs i < kOmegaPairs
+// (rotary slices up to 256 channels).
+constexpr int kOmegaPairs = 128;
+struct OmegaTable {
+    double w[kOmegaPairs];
+};
+
+// cos and sin of delta*omega.  The argument is formed and reduced by pi/2 in
+// fp64; sin and cos of the reduced angle r (|r| <= pi/4) are the Taylor series
+//   sin r = r - r^3/3! + r^5/5! - r^7/7! + r^9/9!
+//   cos r = 1 - r^2/2! + r^4/4! - r^6/6! + r^8/8! - r^10/10!
+// evaluated by Horner's rule in fp32; the quadrant picks signs and swaps.
+__device__ inline void delta_sincos(int64_t delta, double omega, float& c, float& s) {
+    static_assert(kOmegaPairs >= kWave, "each lane of a wave reads one table entry");
+    const double x = (double)delta * omega;
+    const double k = rint(x * 0.63661977236758134308);            // 2/pi
+    double r = fma(-k, 1.5707963267948966192, x);                // pi/2, leading part
+    r = fma(-k, 6.123233995736766036e-17, r);                    // pi/2, trailing part
+    const float f = (float)r;
+    const float z = f * f;
+    float ps = fmaf(z, 2.75573192e-6f, -1.98412698e-4f);          // 1/9!, -1/7!
+    ps = fmaf(z, ps, 8.33333333e-3f);                             // 1/5!
+    ps = fmaf(z, ps, -0.166666667f);                              // -1/3!
+    const float sr = fmaf(f * z, ps, f);
+    float pc = fmaf(z, -2.75573192e-7f, 2.48015873e-5f);          // -1/10!, 1/8!
+    pc = fmaf(z, pc, -1.38888889e-3f);                            // -1/6!
+    pc = fmaf(z, pc, 4.16666667e-2f);                             // 1/4!
+    pc = fmaf(z, pc, -0.5f);                                      // -1/2!
+    const float cr = fmaf(z, pc, 1.0f);
+    const int q = (int)((int64_t)k & 3);
+    const float sa = (q & 1) ? cr : sr;
+    const float ca = (q & 1) ? sr : cr;
+    s = (q & 2) ? -sa : sa;
+    c = ((q + 1) & 2) ? -ca : ca;
+}
 
 __device__ inline void rot(float a, float b, float c, float s, float& ra, float& rb) {
     ra = fmaf(a, c, -(b * s));
@@ -135,38 +186,59 @@ __device__ inline void rotate_chunks(u32x4& x, u32x4& y, const float* c, const f
     }
 }
 
-template <int EB, int STYLE, bool SEG>
-__global__ __launch_bounds__(256) void splice_kernel(SpliceArgs a, Geo g) {
-    constexpr int CE = 16 / EB;   // elements per 16-byte chunk = pairs per rotary lane
-    const int tid = threadIdx.x;
-    const int tl = tid / g.lanes;
-    const int lane = tid - tl * g.lanes;
-    if (tl >= g.tok_per_block) return;
-    const int64_t t = (int64_t)blockIdx.x * g.tok_per_block + tl;
+// Pair index of coefficient j of rotary lane l (HALF: the lane's chunk holds CE
+// consecutive pairs; INTERLEAVED: each of its two chunks holds CE/2 pairs).
+template <int CE, int STYLE>
+__device__ inline int lane_pair(int l, int j, int half_r) {
+    if constexpr (STYLE == kHalf)
+        return l * CE + j;
+    else
+        return j < CE / 2 ? l * (CE / 2) + j : (half_r + l) * (CE / 2) + (j - CE / 2);
+}
 
-    int64_t src_slot, dst_slot, delta;
-    bool valid;
+template <int EB, int STYLE, bool SEG>
+__global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, OmegaTable om) {
+    constexpr int CE = 16 / EB;   // elements per 16-byte chunk = pairs per rotary lane
+    // Token tile.  Workgroups are dealt to the XCDs round-robin; when the tile
+    // count divides evenly, renumber the tiles so that each XCD streams one
+    // contiguous range of tokens of the row group instead of every eighth tile.
+    uint32_t tile = blockIdx.x;
+    if (g.xcd_tiles) tile = (tile % kXcds) * g.xcd_tiles + tile / kXcds;
+    const int grp = blockIdx.y;
+
+    const uint32_t tid = threadIdx.x;
+    const uint32_t tl = g.lanes == 1 ? tid : __umulhi(tid, g.lanes_magic);   // tid / lanes, exact here
+    const int lane = (int)(tid - tl * (uint32_t)g.lanes);
+    const int64_t t = (int64_t)tile * g.tok_per_block + tl;
+
+    // The prologue is straight-line and issues its loads in the order their
+    // results are needed: positions, then this lane's frequency, then the K/V
+    // rows.  Memory counters retire in order, so waiting for the positions and
+    // the frequency leaves the K/V loads in flight while the coefficients are
+    // formed.  Lanes and rows without work load from a clamped, in-range
+    // address and store nothing; they stay to the end because the wave shares
+    // its coefficients through shuffles.
+    int64_t src_slot, dst_slot = -1, delta = 0;
+    bool present = (int)tl < g.tok_per_block;   // a token of the chunk (or segment)
+    bool active;                                // ... whose source row can be read
+    int32_t dp = 0, spos = 0;
     if constexpr (SEG) {
         const SpliceSegment sg = a.segs[blockIdx.z];
-        if (t >= sg.n_tokens) return;
         src_slot = sg.src_slot0 + t;
+        present = present && t < sg.n_tokens;
+        active = present && src_slot >= 0 && src_slot < a.n_tokens;
         const int64_t p = (int64_t)sg.dst_pos0 + t;
-        dst_slot = sg.dst_seq_base + p;
+        if (p >= 0 && p < sg.dst_seq_len) dst_slot = sg.dst_seq_base + p;
         delta = (int64_t)sg.dst_pos0 - (int64_t)sg.src_pos0;
-        valid = src_slot >= 0 && src_slot < a.n_tokens && p >= 0 && p < sg.dst_seq_len &&
-                dst_slot >= 0 && dst_slot < a.dst_capacity;
+        if (!active) src_slot = 0;
     } else {
-        if (t >= a.n_tokens) return;
-        src_slot = t;
-        const int32_t dp = a.dst_pos[t];
-        dst_slot = dp;
-        delta = (int64_t)dp - (int64_t)a.src_pos[t];
-        valid = dst_slot >= 0 && dst_slot < a.dst_capacity;
+        present = present && t < a.n_tokens;
+        active = present;
+        src_slot = active ? t : a.n_tokens - 1;
+        dp = a.dst_pos[src_slot];
+        spos = a.src_pos[src_slot];
     }
-    if (!valid) {
-        if (lane == 0 && blockIdx.y == 0 && a.err_flag) atomicOr(a.err_flag, 1);
-        return;
-    }
+    const double w_lane = om.w[__lane_id()];   // pair lane_id's frequency (used when n_pairs <= 64)
 
     // This lane's two chunks and whether they rotate.
     const bool is_k = lane < g.lanes_k;
@@ -190,70 +262,105 @@ __global__ __launch_bounds__(256) void splice_kernel(SpliceArgs a, Geo g) {
         ca = m;
         cb = m + (g.n_vc >> 1);
     }
-    rope = rope && delta != 0;
-
-    float cs[CE], sn[CE];
-    if (rope) {
-        const double inv_r = 1.0 / (double)a.rope_dim;
-#pragma unroll
-        for (int j = 0; j < CE; ++j) {
-            int pair;
-            if constexpr (STYLE == kHalf)
-                pair = lane * CE + j;
-            else
-                pair = j < CE / 2 ? lane * (CE / 2) + j : (half_r + lane) * (CE / 2) + (j - CE / 2);
-            const double w = pow(a.theta, -2.0 * (double)pair * inv_r);
-            double sd, cd;
-            sincos((double)delta * w, &sd, &cd);
-            cs[j] = (float)cd;
-            sn[j] = (float)sd;
-        }
-    }
 
     const int64_t s0 = is_k ? a.src_k_stride[0] : a.src_v_stride[0];
     const int64_t s1 = is_k ? a.src_k_stride[1] : a.src_v_stride[1];
     const int64_t s2 = is_k ? a.src_k_stride[2] : a.src_v_stride[2];
     const int64_t d0 = is_k ? a.dst_k_stride[0] : a.dst_v_stride[0];
     const int64_t d1 = is_k ? a.dst_k_stride[1] : a.dst_v_stride[1];
-    const int64_t d2 = is_k ? a.dst_k_stride[2] : a.dst_v_stride[2];
-    const char* sbase = (is_k ? a.src_k : a.src_v) + src_slot * s2 * EB;
-    char* dbase = (is_k ? a.dst_k : a.dst_v) + dst_slot * d2 * EB;
-    const int oa = ca * 16, ob = cb * 16;
+    const char* sbase = (is_k ? a.src_k : a.src_v) + src_slot * s2 * EB + ca * 16;
+    const int ob = (cb - ca) * 16;
 
-    const int r0 = blockIdx.y * g.rows_per_block;
+    // Rows r0..r1 of this block, walked as (layer, head) without division;
+    // rows past r1 in the last unrolled step load row r1 - 1 again.
+    const int r0 = grp * g.rows_per_block;
     const int r1 = min(r0 + g.rows_per_block, g.n_rows);
-    for (int r = r0; r < r1; r += kUnroll) {
-        u32x4 va[kUnroll], vb[kUnroll];
-        int64_t doff[kUnroll];
+    int layer = r0 / a.n_kv_heads;
+    int head = r0 - layer * a.n_kv_heads;
+    const int last_layer = (r1 - 1) / a.n_kv_heads;
+    const int last_head = (r1 - 1) - last_layer * a.n_kv_heads;
+
+    u32x4 va[kUnroll], vb[kUnroll];
+    int64_t doff[kUnroll];
+    auto load_rows = [&](int r) __attribute__((always_inline)) {
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const int rr = r + u;
-            if (rr < r1) {
-                const int layer = rr / a.n_kv_heads;
-                const int head = rr - layer * a.n_kv_heads;
-                const int64_t so = ((int64_t)layer * s0 + (int64_t)head * s1) * EB;
-                doff[u] = ((int64_t)layer * d0 + (int64_t)head * d1) * EB;
-                va[u] = ld16(sbase + so + oa);
-                vb[u] = ld16(sbase + so + ob);
+            const bool in = r + u < r1;
+            const int l = in ? layer : last_layer, h = in ? head : last_head;
+            doff[u] = ((int64_t)l * d0 + (int64_t)h * d1) * EB;
+            const char* sp = sbase + ((int64_t)l * s0 + (int64_t)h * s1) * EB;
+            va[u] = ld16(sp);
+            vb[u] = ld16(sp + ob);
+            if (++head == a.n_kv_heads) {
+                head = 0;
+                ++layer;
             }
         }
+    };
+    load_rows(r0);
+
+    if constexpr (!SEG) {
+        dst_slot = dp;
+        delta = (int64_t)dp - (int64_t)spos;
+    }
+    const bool valid = dst_slot >= 0 && dst_slot < a.dst_capacity;
+    const bool work = active && valid;
+
+    // Rotation coefficients.  When every working lane of the wave has the same
+    // delta (always so in segment mode; so for a contiguous chunk in token
+    // mode), lane j evaluates pair j once and rotary lanes gather theirs by
+    // shuffle; otherwise each rotary lane evaluates its own CE pairs.
+    float cs[CE], sn[CE];
+    const int32_t d_ref = __shfl((int32_t)delta, 0);
+    const bool uniform = __all(!work || delta == (int64_t)d_ref) && g.n_pairs <= kWave;
+    if (uniform) {
+        if (d_ref != 0) {
+            float c1 = 1.0f, s1v = 0.0f;
+            if (__lane_id() < g.n_pairs) delta_sincos(d_ref, w_lane, c1, s1v);
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            if (r + u < r1) {
-                if (rope) rotate_chunks<EB, STYLE>(va[u], vb[u], cs, sn);
-                st16(dbase + doff[u] + oa, va[u]);
-                st16(dbase + doff[u] + ob, vb[u]);
+            for (int e = 0; e < CE; ++e) {
+                const int src = rope ? lane_pair<CE, STYLE>(lane, e, half_r) : 0;
+                cs[e] = __shfl(c1, src);
+                sn[e] = __shfl(s1v, src);
             }
+        }
+        rope = rope && d_ref != 0;
+    } else {
+        rope = rope && delta != 0;
+        if (rope) {
+#pragma unroll
+            for (int e = 0; e < CE; ++e)
+                delta_sincos(delta, om.w[lane_pair<CE, STYLE>(lane, e, half_r)], cs[e], sn[e]);
         }
     }
+
+    if (work) {
+        char* dbase = (is_k ? a.dst_k : a.dst_v) +
+                      dst_slot * (is_k ? a.dst_k_stride[2] : a.dst_v_stride[2]) * EB + ca * 16;
+        for (int r = r0;;) {
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                if (r + u < r1) {
+                    if (rope) rotate_chunks<EB, STYLE>(va[u], vb[u], cs, sn);
+                    st16(dbase + doff[u], va[u]);
+                    st16(dbase + doff[u] + ob, vb[u]);
+                }
+            }
+            r += kUnroll;
+            if (r >= r1) break;
+            load_rows(r);
+        }
+    }
+    if (present && !work && lane == 0 && grp == 0 && a.err_flag) atomicOr(a.err_flag, 1);
 }
 
 template <int EB, int STYLE>
-hipError_t launch_typed(const SpliceArgs& a, const Geo& g, dim3 grid, dim3 block, hipStream_t st) {
+hipError_t launch_typed(const SpliceArgs& a, const Geo& g, const OmegaTable& om, dim3 grid, dim3 block,
+                        hipStream_t st) {
     if (a.segs)
-        hipLaunchKernelGGL((splice_kernel<EB, STYLE, true>), grid, block, 0, st, a, g);
+        hipLaunchKernelGGL((splice_kernel<EB, STYLE, true>), grid, block, 0, st, a, g, om);
     else
-        hipLaunchKernelGGL((splice_kernel<EB, STYLE, false>), grid, block, 0, st, a, g);
+        hipLaunchKernelGGL((splice_kernel<EB, STYLE, false>), grid, block, 0, st, a, g, om);
     return hipGetLastError();
 }
 
@@ -266,10 +373,11 @@ hipError_t launch_splice(const SpliceArgs& a, hipStream_t stream) {
     g.n_vc = a.v_dim / ce;
     g.rope_c0 = a.rope_offset / ce;
     g.rope_nc = a.rope_dim / ce;
+    g.n_pairs = a.rope_dim / 2;
     g.lanes_k = g.n_kc / 2;
     g.lanes_v = g.n_vc / 2;
     g.lanes = g.lanes_k + g.lanes_v;
-    g.tok_per_block = g.lanes >= 256 ? 1 : 256 / g.lanes;
+    g.tok_per_block = g.lanes >= kBlock ? 1 : kBlock / g.lanes;
     g.n_rows = a.n_layers * a.n_kv_heads;
 
     const bool seg = a.segs != nullptr;
@@ -281,23 +389,26 @@ hipError_t launch_splice(const SpliceArgs& a, hipStream_t stream) {
     const int64_t nz = seg ? a.n_segs : 1;
     if (tokens <= 0 || nz <= 0 || g.n_rows <= 0) return hipSuccess;
 
-    const int64_t gx = (tokens + g.tok_per_block - 1) / g.tok_per_block;
-    // Enough blocks to fill 256 CUs several times over, while every thread
-    // still visits several rows so its cos/sin are reused.
-    int64_t want_y = (PKV_SPLICE_TARGET_BLOCKS + gx * nz - 1) / (gx * nz);
-    if (want_y < 1) want_y = 1;
-    int rows = (int)((g.n_rows + want_y - 1) / want_y);
-    rows = rows < PKV_SPLICE_MIN_ROWS ? (g.n_rows < PKV_SPLICE_MIN_ROWS ? g.n_rows : PKV_SPLICE_MIN_ROWS) : rows;
-    g.rows_per_block = rows;
-    const int gy = (g.n_rows + rows - 1) / rows;
+    if (g.n_pairs > kOmegaPairs) return hipErrorInvalidValue;
+    g.rows_per_block = g.n_rows < kRowsPerBlock ? g.n_rows : kRowsPerBlock;
+    const int64_t n_tiles = (tokens + g.tok_per_block - 1) / g.tok_per_block;
+    const int64_t n_groups = (g.n_rows + g.rows_per_block - 1) / g.rows_per_block;
+    if (n_tiles > 0x7fffffff || n_groups > 65535 || nz > 65535) return hipErrorInvalidConfiguration;
+    g.xcd_tiles = n_tiles % kXcds == 0 ? (int)(n_tiles / kXcds) : 0;
+    g.lanes_magic = g.lanes > 1 ? (uint32_t)((0x100000000ull + g.lanes - 1) / g.lanes) : 0;   // ceil(2^32/lanes)
 
-    dim3 grid((unsigned)gx, (unsigned)gy, (unsigned)nz);
-    dim3 block((unsigned)(g.tok_per_block * g.lanes));
+    OmegaTable om;
+    const int n_pairs = a.rope_dim / 2;
+    for (int i = 0; i < kOmegaPairs; ++i)
+        om.w[i] = i < n_pairs ? pow(a.theta, -2.0 * (double)i / (double)a.rope_dim) : 0.0;
+
+    dim3 grid((unsigned)n_tiles, (unsigned)n_groups, (unsigned)nz);
+    dim3 block((unsigned)kBlock);
     if (a.elem_bytes == 2)
-        return a.rope_style == kHalf ? launch_typed<2, 0>(a, g, grid, block, stream)
-                                     : launch_typed<2, 1>(a, g, grid, block, stream);
-    return a.rope_style == kHalf ? launch_typed<4, 0>(a, g, grid, block, stream)
-                                 : launch_typed<4, 1>(a, g, grid, block, stream);
+        return a.rope_style == kHalf ? launch_typed<2, 0>(a, g, om, grid, block, stream)
+                                     : launch_typed<2, 1>(a, g, om, grid, block, stream);
+    return a.rope_style == kHalf ? launch_typed<4, 0>(a, g, om, grid, block, stream)
+                                 : launch_typed<4, 1>(a, g, om, grid, block, stream);
 }
 
 }  // namespace pkv

@@ -81,6 +81,7 @@ def splice(L, sk=SK, sv=SV, dk=DK, dv=DV, sp=SP, dp=DP, theta=1e4, r=128):
     (dict(rope_style=3), {}, pkv.PKV_ERR_UNSUPPORTED),
     ({}, dict(r=8), pkv.PKV_ERR_UNSUPPORTED),               # rope_dim not a multiple of 16 (bf16)
     (dict(head_dim=120, v_dim=120), dict(r=96), pkv.PKV_ERR_UNSUPPORTED),
+    (dict(head_dim=512, v_dim=512), dict(r=288), pkv.PKV_ERR_UNSUPPORTED),   # rotary slice > 256 channels
     ({}, dict(sk=SK + 8), pkv.PKV_ERR_ALIGN),
     (dict(src_k_stride=pkv._i64x3(4 * 16 * 128, 16 * 128, 132)), {}, pkv.PKV_ERR_ALIGN),
     ({}, dict(dk=SK + 4096), pkv.PKV_ERR_ALIAS),             # dst_k partially overlaps src_k

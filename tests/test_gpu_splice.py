@@ -115,6 +115,48 @@ def test_small_bf16(case):
     log("  elements not bit-equal:", n_diff, "needing the floor:", n_floor)
 
 
+@pytest.mark.parametrize("style", [0, 1])
+@pytest.mark.parametrize("d,v_dim,rope_dim,rope_offset", [(128, 128, 128, 0), (576, 0, 64, 512)])
+def test_scattered_positions(style, d, v_dim, rope_dim, rope_offset):
+    """Per-token source and destination positions with no common delta (every wave takes the per-lane
+    coefficient path), destinations a random permutation of a larger cache, token count not a tile multiple."""
+    n, cap, L, Hkv = 333, 1500, 2, (2 if v_dim else 1)
+    rng = np.random.default_rng(11 + style)
+    g = synth.Draws(12, "cpu")
+    skill_k = host_bits(g.normal((L, Hkv, n, d)))
+    skill_v = host_bits(g.normal((L, Hkv, n, v_dim))) if v_dim else None
+    ctx_k = host_bits(g.normal((L, Hkv, cap, d)))
+    ctx_v = host_bits(g.normal((L, Hkv, cap, v_dim))) if v_dim else None
+    src = rng.integers(-40000, 40000, n).astype(np.int32)
+    dst = rng.permutation(cap)[:n].astype(np.int32)
+    w = synth.Workload("scatter", L, Hkv, Hkv, d, v_dim, 5e5, rope_dim, rope_offset, style, "bf16", n, 0, 0, cap,
+                       1, 1.0, mla=not v_dim)
+    log("scattered positions", dict(style=style, d=d, rope_dim=rope_dim))
+    gk, gv = run_gpu_splice(w, skill_k, skill_v, ctx_k, ctx_v, src, dst)
+    ok, ov = oracle_splice(w, skill_k, skill_v, ctx_k, ctx_v, src, dst)
+    if ov is not None:
+        np.testing.assert_array_equal(gv, ov)
+    np.testing.assert_array_equal(gk[..., :rope_offset], ok[..., :rope_offset])
+    compare(w, gk, gv, ok, ov)
+
+
+def test_scattered_positions_fp32():
+    n, cap, L, Hkv, d = 200, 700, 1, 2, 64
+    rng = np.random.default_rng(5)
+    g = synth.Draws(13, "cpu")
+    skill_k = g.normal((L, Hkv, n, d), torch.float32).numpy()
+    skill_v = g.normal((L, Hkv, n, d), torch.float32).numpy()
+    ctx_k = g.normal((L, Hkv, cap, d), torch.float32).numpy()
+    ctx_v = g.normal((L, Hkv, cap, d), torch.float32).numpy()
+    src = rng.integers(0, 20000, n).astype(np.int32)
+    dst = rng.permutation(cap)[:n].astype(np.int32)
+    w = synth.Workload("scatter32", L, Hkv, Hkv, d, d, 1e4, d, 0, synth.HALF, "f32", n, 0, 0, cap, 1, 1.0)
+    gk, gv = run_gpu_splice(w, skill_k, skill_v, ctx_k, ctx_v, src, dst)
+    ok, ov = oracle_splice(w, skill_k, skill_v, ctx_k, ctx_v, src, dst)
+    np.testing.assert_array_equal(gv.view(np.uint32), ov.view(np.uint32))
+    compare(w, gk, gv, ok, ov)
+
+
 def test_mla_rows_small():
     w = synth.Workload("mla_small", 3, 16, 1, 576, 512, 1e4, 64, 512, synth.INTERLEAVED, "bf16", 150, 0, 900,
                        1200, 4, 1 / 192 ** 0.5, mla=True)
