@@ -218,6 +218,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=30)
+    ap.add_argument("--min-warmup-s", type=float, default=0.25,
+                    help="keep warming up until this much wall time has passed (clock ramp)")
     ap.add_argument("--workload", default="gqa8b", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--splits", type=int, default=0, help="KV splits for attention (0 = library choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -243,9 +245,17 @@ def main():
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
 
-    for _ in range(args.warmup):
+    # Untimed warm-up: the requested steps, continued until at least
+    # --min-warmup-s of GPU work has run, so the shader clock has left its
+    # idle state before the timed region (a few ms of work is not enough).
+    t_warm = time.perf_counter()
+    n_warm = 0
+    while n_warm < args.warmup or time.perf_counter() - t_warm < args.min_warmup_s:
         step.splice(sh)
         step.attention(sh)
+        n_warm += 1
+        if n_warm % 16 == 0:
+            torch.cuda.synchronize()
     torch.cuda.synchronize()
 
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
@@ -300,6 +310,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "warmup_steps_run": n_warm,
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "weak",

@@ -177,13 +177,13 @@ Plan make_plan(const AttnArgs& a, int splits) {
     return p;
 }
 
-// Workgroups that fit on one CU at once (LDS bound).
+// Workgroups that fit on one CU at once (LDS and register bound).
 int wgs_per_cu(const AttnArgs& a, const Plan& p) {
-    int lds;
-    if (a.variant == 1) lds = p.ns * 32 * 576 * 2 + 16 * 1024;
-    else lds = p.ns * 2 * (p.ns == 4 ? 32 : 64) * a.head_dim * 2;
-    const int n = (160 * 1024) / (lds > 0 ? lds : 1);
-    return n < 1 ? 1 : n;
+    if (a.variant == 1) return 1;                     // MLA: 36 KB stages plus the score exchange
+    const int tile = p.ns == 4 ? 32 : 64;             // keys per K/V tile
+    const int lds = p.ns * 2 * tile * a.head_dim * 2;
+    const int n = (160 * 1024) / lds;
+    return n < 1 ? 1 : (n > 2 ? 2 : n);               // two waves per SIMD at most (registers)
 }
 
 }  // namespace

@@ -67,7 +67,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
     constexpr int DB = D / 32;             // 32-channel output blocks
     constexpr int TE = BN * D;             // elements of one K or V tile
     static_assert(2 * KBLK % NW == 0, "tile loads must split evenly over the waves");
-    static_assert(NS >= 2 && NS <= 4, "2..4 stages");
+    static_assert(NS >= 2 && NS <= 10 && (NS - 2) * PER < 64, "2..10 stages within the vmcnt range");
 
     // One LDS block: NS K stages, then NS V stages.  Stage offsets are
     // compile-time constants after unrolling, so one address register per
@@ -349,12 +349,17 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
     };
 
     // Tiles are staged through NS LDS stages: tile i lives in stage i % NS
-    // and is issued NS-1 tiles ahead of its use.
+    // and is issued NS-1 tiles ahead of its use.  Wait until at most
+    // tiles_after later tiles (at most NS-2) are still in flight.
     auto wait_outstanding = [&](int tiles_after) __attribute__((always_inline)) {
-        if (NS > 3 && tiles_after >= 3) wait_vmcnt<(NS > 3 ? 3 : 1) * PER>();
-        else if (NS > 2 && tiles_after >= 2) wait_vmcnt<(NS > 2 ? 2 : 1) * PER>();
-        else if (tiles_after == 1) wait_vmcnt<PER>();
-        else wait_vmcnt<0>();
+        if (tiles_after >= NS - 2) {
+            wait_vmcnt<(NS - 2) * PER>();
+        } else {
+            static_for<0, NS - 2>([&](auto k_tag) {
+                constexpr int K = decltype(k_tag)::value;
+                if (tiles_after == K) wait_vmcnt<K * PER>();
+            });
+        }
     };
     auto lds_reads_done = []() __attribute__((always_inline)) { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14)); };
 
@@ -382,7 +387,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
         pv(vst(S), pb);
     };
     auto plain_from = [&](int first) __attribute__((always_inline)) {
-        for (int t = first & ~(NS - 1); t < n_tiles; t += NS) {
+        for (int t = first - first % NS; t < n_tiles; t += NS) {
             static_for<0, NS>([&](auto s_tag) {
                 const int i = t + decltype(s_tag)::value;
                 if (i >= first && i < n_tiles) plain_tile(i, s_tag);
@@ -411,7 +416,8 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
         // never wait at each other's barriers.  Iteration t reads K of tile
         // t+1 and V of tile t; tile t+3 is issued after the barrier opening
         // it, into the stage that tile t-1 left.
-        static_assert(NS == 4 && NKB == 1, "the pipelined schedule uses four LDS stages of 32-key tiles");
+        static_assert(NS >= 4 && NS % 2 == 0 && NKB == 1,
+                      "the pipelined schedule uses an even number (>= 4) of LDS stages of 32-key tiles");
         const int F = sc2 > 0.f ? max(0, min(n_tiles, (e_min - k_begin) / BN)) : 0;
         const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
@@ -536,11 +542,11 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
 
         auto iteration = [&](int i, auto u_tag, f32x16 (&cur)[QB], f32x16 (&nxt)[QB]) __attribute__((always_inline)) {
             constexpr int U = decltype(u_tag)::value;
-            if (i + 2 < n_tiles) wait_vmcnt<PER>();
-            else wait_vmcnt<0>();
+            wait_outstanding(min(i + NS - 2, n_tiles - 1) - (i + 1));   // tile i+1 has landed
             lds_reads_done();
             bare_barrier();
-            if (i + 3 < n_tiles) issue(k_begin + (i + 3) * BN, kst((U + 3) % NS), vst((U + 3) % NS));
+            if (i + NS - 1 < n_tiles)
+                issue(k_begin + (i + NS - 1) * BN, kst((U + NS - 1) % NS), vst((U + NS - 1) % NS));
             half_step(kst((U + 1) % NS), 0, vst(U), 0, cur, nxt);
         };
 
@@ -550,7 +556,8 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
             constexpr int U = decltype(u_tag)::value;
             lds_reads_done();
             bare_barrier();
-            if (i + 3 < n_tiles) issue(k_begin + (i + 3) * BN, kst((U + 3) % NS), vst((U + 3) % NS));
+            if (i + NS - 1 < n_tiles)
+                issue(k_begin + (i + NS - 1) * BN, kst((U + NS - 1) % NS), vst((U + NS - 1) % NS));
             bf16x8 pb[QB][2];
 #pragma unroll
             for (int qb = 0; qb < QB; ++qb) {
@@ -620,12 +627,13 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
                 });
             }
             const int last = F - 1;
-            switch (last & 3) {
-                case 0: drain(last, std::integral_constant<int, 0>{}, sA); break;
-                case 1: drain(last, std::integral_constant<int, 1>{}, sB); break;
-                case 2: drain(last, std::integral_constant<int, 2>{}, sA); break;
-                default: drain(last, std::integral_constant<int, 3>{}, sB); break;
-            }
+            static_for<0, NS>([&](auto u_tag) {
+                constexpr int u = decltype(u_tag)::value;
+                if (last % NS == u) {
+                    if constexpr (u % 2 == 0) drain(last, u_tag, sA);
+                    else drain(last, u_tag, sB);
+                }
+            });
         }
         plain_from(F >= 2 ? F : 0);
     }
