@@ -98,11 +98,172 @@ class GqaStep:
     def splice_bytes(self):
         return self.w.splice_bytes()
 
+    def describe(self):
+        w = self.w
+        return ("%s: %d layers, %d/%d heads, d %d, %d-token skill %d->%d, %d-token suffix over %d slots"
+                % (w.name, w.n_layers, w.n_heads, w.n_kv_heads, w.head_dim, w.skill_tokens, w.src_pos0, w.dst_pos0,
+                   w.n_q, w.kv_len))
+
     def attn_flops(self):
         return self.w.attn_flops()
 
     def attn_bytes(self):
         return self.w.attn_bytes()
+
+
+class BatchedStep:
+    """Batched composition: 16 sequences each splice the same three library skills
+    (1024, 2048, 4096 tokens) at their own offsets, then run a 256-query causal
+    suffix over their own cache length (ragged).  One splice launch covers all
+    48 segments and one attention launch covers all sequences and layers."""
+
+    def __init__(self, bw: synth.BatchedWorkload, n_splits: int, seed: int = 0):
+        self.bw = bw
+        dev = torch.device("cuda")
+        self.plan = plan = synth.batched_plan(bw, seed)
+        c = synth.batched_case(bw, plan, seed=seed, device=dev)
+        self.cache_k, self.cache_v = c["ctx_k"], c["ctx_v"]
+        L, Hkv, H, d, nq = bw.n_layers, bw.n_kv_heads, bw.n_heads, bw.head_dim, bw.n_q
+        n_seqs = bw.n_seqs
+        # Post-RoPE library keys: skill k's tokens sit at positions src_pos0[k] + t.
+        self.skill_v = c["skill_v"]
+        self.skill_k = torch.empty_like(c["skill_k_pre"])
+        lib_segs = [dict(src_slot0=plan["skill_base"][k], dst_seq_base=plan["skill_base"][k] - plan["src_pos0"][k],
+                         n_tokens=bw.skills[k], src_pos0=0, dst_pos0=plan["src_pos0"][k],
+                         dst_seq_len=plan["src_pos0"][k] + bw.skills[k]) for k in range(len(bw.skills))]
+        pkv.reposition_splice_batched(c["skill_k_pre"], None, self.skill_k, None, pkv.make_segments(lib_segs, dev),
+                                      len(lib_segs), max(bw.skills), bw.theta, d)
+        del c["skill_k_pre"]
+        # Suffix keys (rotated to their positions) and values into each sequence's cache slots.
+        suf_segs, q_segs, q_pos, cu, bases, kvl = [], [], [], [0], [], []
+        for s_i, sq in enumerate(plan["seqs"]):
+            C = sq["ctx"]
+            suf_segs.append(dict(src_slot0=s_i * nq, dst_seq_base=sq["seq_base"], n_tokens=nq, src_pos0=0,
+                                 dst_pos0=C, dst_seq_len=sq["kv_len"]))
+            q_segs.append(dict(src_slot0=s_i * nq, dst_seq_base=s_i * nq - C, n_tokens=nq, src_pos0=0, dst_pos0=C,
+                               dst_seq_len=C + nq))
+            q_pos.extend(range(C, C + nq))
+            cu.append(cu[-1] + nq)
+            bases.append(sq["seq_base"])
+            kvl.append(sq["kv_len"])
+            self.cache_v[:, :, sq["seq_base"] + C: sq["seq_base"] + C + nq] = c["suf_v"][:, :, s_i * nq:(s_i + 1) * nq]
+        pkv.reposition_splice_batched(c["suf_k_pre"], None, self.cache_k, None, pkv.make_segments(suf_segs, dev),
+                                      len(suf_segs), nq, bw.theta, d)
+        # Post-RoPE queries [L][rows][H][d], rotated through a [L][H][rows][d] view.
+        self.q = torch.empty_like(c["q_pre"])
+        pkv.reposition_splice_batched(c["q_pre"].permute(0, 2, 1, 3), None, self.q.permute(0, 2, 1, 3), None,
+                                      pkv.make_segments(q_segs, dev), len(q_segs), nq, bw.theta, d)
+        del c
+        self.segs = synth.batched_segments(plan)
+        self.segs_dev = pkv.make_segments(self.segs, dev)
+        self.max_seg = max(sg["n_tokens"] for sg in self.segs)
+        self.q_pos = torch.tensor(q_pos, dtype=torch.int32, device=dev)
+        self.cu_q = torch.tensor(cu, dtype=torch.int32, device=dev)
+        self.kv_base = torch.tensor(bases, dtype=torch.int64, device=dev)
+        self.kv_len = torch.tensor(kvl, dtype=torch.int32, device=dev)
+        self.out = torch.zeros(L, n_seqs * nq, H, d, dtype=torch.bfloat16, device=dev)
+        self.splice_layout = pkv.make_layout(self.skill_k, self.skill_v, self.cache_k, self.cache_v)
+        self.desc = pkv.make_attn_desc(self.q, self.cache_k, self.cache_v, self.out, max(kvl), n_seqs=n_seqs,
+                                       cu_q=self.cu_q, kv_base=self.kv_base, max_q=nq, n_splits=n_splits)
+        self.ws_bytes = pkv.pkv_attention_workspace_size(self.desc, H, Hkv, d)
+        self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device=dev)
+        torch.cuda.synchronize()
+
+    def splice(self, stream):
+        bw = self.bw
+        st = pkv.pkv_reposition_splice_batched(self.skill_k, self.skill_v, self.cache_k, self.cache_v, self.segs_dev,
+                                               len(self.segs), self.max_seg, bw.theta, bw.head_dim,
+                                               self.splice_layout, stream)
+        if st != 0:
+            raise pkv.PkvError(st, pkv.pkv_last_error())
+
+    def attention(self, stream):
+        bw = self.bw
+        st = pkv.pkv_suffix_attention(self.q, self.cache_k, self.cache_v, self.out, self.q_pos, self.kv_len,
+                                      bw.n_heads, bw.n_kv_heads, bw.head_dim, bw.scale, self.desc, self.ws,
+                                      self.ws_bytes, stream)
+        if st != 0:
+            raise pkv.PkvError(st, pkv.pkv_last_error())
+
+    def splice_bytes(self):
+        return synth.batched_splice_bytes(self.bw, self.plan)
+
+    def attn_flops(self):
+        return synth.batched_attn_flops(self.bw, self.plan)
+
+    def attn_bytes(self):
+        return synth.batched_attn_bytes(self.bw, self.plan)
+
+    def describe(self):
+        bw = self.bw
+        ctx = [sq["ctx"] for sq in self.plan["seqs"]]
+        return ("batched: %d layers, %d/%d heads, d %d, %d sequences x skills %s at random offsets in %d-%d-token "
+                "contexts, %d-query ragged suffixes" % (bw.n_layers, bw.n_heads, bw.n_kv_heads, bw.head_dim,
+                                                        bw.n_seqs, "/".join(map(str, bw.skills)), min(ctx), max(ctx),
+                                                        bw.n_q))
+
+
+def cpu_baseline_batched(bw: synth.BatchedWorkload, budget_s: float = 10.0):
+    """Time the fp64 oracle on a bounded sample of the batched workload: the three
+    segments of sequence 0 for as many single-layer passes as fit in half the
+    budget (scaled to all 48 segments and 32 layers by bytes), and layer 0 of
+    sequence 0's suffix attention for as many queries as fit in the other half
+    (scaled by visible pairs)."""
+    import numpy as np
+
+    import oracle
+
+    oracle.build(force=False)
+    threads = oracle.max_threads()
+    bits = synth.to_numpy_bits
+    plan = synth.batched_plan(bw, 0)
+    c = synth.batched_case(bw, plan, seed=1, layers=1)
+    sk, sv = bits(c["skill_k_pre"]), bits(c["skill_v"])
+    sq = plan["seqs"][0]
+    seq_k = bits(c["ctx_k"])[:, :, sq["seq_base"]: sq["seq_base"] + sq["kv_len"]].copy()
+    seq_v = bits(c["ctx_v"])[:, :, sq["seq_base"]: sq["seq_base"] + sq["kv_len"]].copy()
+
+    def run_seq0():
+        for sg in sq["segs"]:
+            n = sg["n_tokens"]
+            sl = slice(sg["src_slot0"], sg["src_slot0"] + n)
+            oracle.reposition_splice(np.ascontiguousarray(sk[:, :, sl]), np.ascontiguousarray(sv[:, :, sl]), seq_k,
+                                     seq_v, np.arange(sg["src_pos0"], sg["src_pos0"] + n, dtype=np.int32),
+                                     np.arange(sg["dst_pos0"], sg["dst_pos0"] + n, dtype=np.int32), bw.theta,
+                                     bw.head_dim)
+
+    t0 = time.perf_counter()
+    run_seq0()
+    t_one = time.perf_counter() - t0
+    reps = max(1, min(64, int(0.5 * budget_s / max(t_one, 1e-4))))
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        run_seq0()
+    t_splice = time.perf_counter() - t0
+    per_pass = sum(2 * 2 * sg["n_tokens"] * bw.n_kv_heads * bw.head_dim * 2 for sg in sq["segs"])
+    sample_bytes = per_pass * reps
+    q = bits(c["q_pre"][0])[: bw.n_q]
+    q_pos = np.arange(sq["ctx"], sq["ctx"] + bw.n_q, dtype=np.int32)
+    t0 = time.perf_counter()
+    oracle.attention(np.ascontiguousarray(q[:1]), seq_k[0], seq_v[0], q_pos[:1], sq["kv_len"], bw.scale)
+    t_row = max(time.perf_counter() - t0, 1e-4)
+    n_rows = max(1, min(bw.n_q, int(0.5 * budget_s / t_row)))
+    t0 = time.perf_counter()
+    oracle.attention(np.ascontiguousarray(q[:n_rows]), seq_k[0], seq_v[0], q_pos[:n_rows], sq["kv_len"], bw.scale)
+    t_attn = time.perf_counter() - t0
+    vis = sum(min(sq["kv_len"], int(q_pos[i]) + 1) for i in range(n_rows))
+    flops_sample = 4 * bw.head_dim * bw.n_heads * vis
+    attn_us_full = t_attn * synth.batched_attn_flops(bw, plan) / flops_sample * 1e6
+    return {
+        "value": round(sample_bytes / t_splice / 1e9, 4),
+        "unit": "GB/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": "splice: %d passes over sequence 0's three segments of one layer (%.3f GB moved) in %.2f s; "
+                  "attention: layer 0, sequence 0, %d of %d queries in %.2f s, scaled to all sequences and layers "
+                  "by visible pairs" % (reps, sample_bytes / 1e9, t_splice, n_rows, bw.n_q, t_attn),
+        "attention_us_extrapolated": round(attn_us_full, 1),
+    }
 
 
 def cpu_baseline(w: synth.Workload, budget_s: float = 10.0):
@@ -220,7 +381,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--min-warmup-s", type=float, default=0.25,
                     help="keep warming up until this much wall time has passed (clock ramp)")
-    ap.add_argument("--workload", default="gqa8b", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--workload", default="gqa8b", choices=sorted(synth.WORKLOADS) + ["batched"])
     ap.add_argument("--splits", type=int, default=0, help="KV splits for attention (0 = library choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
@@ -239,9 +400,13 @@ def main():
         return
     pkv.lib()   # fail loudly if libpkv.so is missing
 
-    w = synth.WORKLOADS[args.workload]
+    if args.workload == "batched":
+        w = synth.BATCHED
+        step = BatchedStep(w, args.splits)
+    else:
+        w = synth.WORKLOADS[args.workload]
+        step = GqaStep(w, args.splits)
     log("workload", w)
-    step = GqaStep(w, args.splits)
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
 
@@ -295,7 +460,8 @@ def main():
     splice_roof = {"bound": "hbm", "achieved": round(splice_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                    "frac": round(splice_gbs / HBM_PEAK_GBS, 4), "traffic": None}
     splice_roof["kernel"] = "splice_kernel"
-    attn_roof["kernel"] = "attn_gqa_bf16" if not w.mla else "attn_mla_bf16"
+    mla = getattr(w, "mla", False)
+    attn_roof["kernel"] = "attn_gqa_bf16" if not mla else "attn_mla_bf16"
     splice_roof["traffic"] = measured_traffic("splice_kernel", w.name)
     attn_roof["traffic"] = measured_traffic(attn_roof["kernel"], w.name)
     splice_roof["algorithmic_bytes"] = step.splice_bytes()
@@ -318,9 +484,7 @@ def main():
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic",
         "config": {
-            "workload": "%s: %d layers, %d/%d heads, d %d, %d-token skill %d->%d, %d-token suffix over %d slots"
-                        % (w.name, w.n_layers, w.n_heads, w.n_kv_heads, w.head_dim, w.skill_tokens, w.src_pos0,
-                           w.dst_pos0, w.n_q, w.kv_len),
+            "workload": step.describe(),
             "splice_bytes": step.splice_bytes(),
             "attention_flops": step.attn_flops(),
             "attention_bytes": step.attn_bytes(),
@@ -338,7 +502,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
-        result["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+        result["cpu_baseline"] = (cpu_baseline_batched(w, args.cpu_budget) if args.workload == "batched"
+                                  else cpu_baseline(w, args.cpu_budget))
     print(json.dumps(result), flush=True)
 
 

@@ -106,7 +106,8 @@ typedef struct pkv_layout {
  *     dst_k[l][h][dst_pos[t]] = R(delta_t) src_k[l][h][t]   (rotary slice; other channels bit-exact)
  *     dst_v[l][h][dst_pos[t]] = src_v[l][h][t]              (bit-exact)
  * src_pos / dst_pos: device int32 [n_tokens], any sign, |delta| < 2^24.
- * Rotation arithmetic: omega_i is computed on the host in fp64; the angle
+ * Rotation arithmetic: omega_i is formed in fp64 (from powers of theta the
+ * host computes in fp64); the angle
  * delta*omega_i is formed and reduced modulo pi/2 in fp64, its cos/sin are
  * evaluated in fp32 (absolute error below 1e-7), and the rotation runs in fp32
  * with one round-to-nearest-even to the storage type.  delta_t == 0 copies the row

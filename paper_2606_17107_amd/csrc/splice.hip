@@ -21,8 +21,9 @@
 //     Lanes of consecutive tokens are consecutive threads, so each load or
 //     store instruction of a wave covers whole 128-byte lines of
 //     token-contiguous caches.
-//   * omega_i = theta^(-2i/r) is tabulated on the host in fp64 and passed in
-//     the kernel arguments.  Each thread forms delta*omega_i in fp64, reduces
+//   * omega_i = theta^(-2i/r) is formed in fp64 from seven powers of theta
+//     the host passes in the kernel arguments.  Each thread forms
+//     delta*omega_i in fp64, reduces
 //     it by pi/2 in fp64 (a two-part pi/2, so the reduced angle is accurate to
 //     ~1e-16 for any |delta| < 2^31), and evaluates sin and cos of the reduced
 //     angle in [-pi/4, pi/4] with their Taylor series in fp32 (truncation error
@@ -62,6 +63,10 @@ constexpr int kBlock = PKV_SPLICE_BLOCK;
 constexpr int kHalf = 0;
 constexpr int kWave = 64;
 constexpr int kXcds = 8;
+#ifndef PKV_SPLICE_SEG_TILES
+#define PKV_SPLICE_SEG_TILES 32   // segment mode: token-tile blocks per (row group, segment)
+#endif
+constexpr int kSegTiles = PKV_SPLICE_SEG_TILES;
 
 __device__ inline u32x4 ld16(const char* p) {
 #if PKV_SPLICE_NONTEMPORAL
@@ -83,6 +88,7 @@ struct Geo {
     int rope_c0, rope_nc, n_kc, n_vc, n_rows, n_pairs;
     int xcd_tiles;          // tiles per XCD when the tile count divides by 8, else 0
     uint32_t lanes_magic;   // ceil(2^32 / lanes)
+    double rho[7];          // theta^(-2*2^b/rope_dim), b = 0..6
 };
 
 __device__ inline float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
@@ -96,12 +102,11 @@ __device__ inline uint32_t bf_rne(float f) {
 }
 __device__ inline uint32_t bf_pack(float lo, float hi) { return bf_rne(lo) | (bf_rne(hi) << 16); }
 
-// Frequencies omega_i = theta^(-2i/r), fp64, for the pairs i < kOmegaPairs
-// (rotary slices up to 256 channels).
-constexpr int kOmegaPairs = 128;
-struct OmegaTable {
-    double w[kOmegaPairs];
-};
+// Frequencies omega_i = theta^(-2i/r) for pairs i < 128 (rotary slices up to
+// 256 channels), formed in fp64 from the seven powers rho_b = theta^(-2*2^b/r)
+// the host passes in: omega_i is the product of rho_b over the set bits b of
+// i (relative error below 1e-15; no memory access).
+constexpr int kPairBits = 7;
 
 // cos and sin of delta*omega.  The argument is formed and reduced by pi/2 in
 // fp64; sin and cos of the reduced angle r (|r| <= pi/4) are the Taylor series
@@ -109,7 +114,6 @@ struct OmegaTable {
 //   cos r = 1 - r^2/2! + r^4/4! - r^6/6! + r^8/8! - r^10/10!
 // evaluated by Horner's rule in fp32; the quadrant picks signs and swaps.
 __device__ inline void delta_sincos(int64_t delta, double omega, float& c, float& s) {
-    static_assert(kOmegaPairs >= kWave, "each lane of a wave reads one table entry");
     const double x = (double)delta * omega;
     const double k = rint(x * 0.63661977236758134308);            // 2/pi
     double r = fma(-k, 1.5707963267948966192, x);                // pi/2, leading part
@@ -130,6 +134,14 @@ __device__ inline void delta_sincos(int64_t delta, double omega, float& c, float
     const float ca = (q & 1) ? sr : cr;
     s = (q & 2) ? -sa : sa;
     c = ((q + 1) & 2) ? -ca : ca;
+}
+
+__device__ inline double pair_omega(int pair, const Geo& g) {
+    double w = 1.0;
+#pragma unroll
+    for (int b = 0; b < kPairBits; ++b)
+        if ((pair >> b) & 1) w *= g.rho[b];
+    return w;
 }
 
 __device__ inline void rot(float a, float b, float c, float s, float& ra, float& rb) {
@@ -197,48 +209,24 @@ __device__ inline int lane_pair(int l, int j, int half_r) {
 }
 
 template <int EB, int STYLE, bool SEG>
-__global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, OmegaTable om) {
+__global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g) {
     constexpr int CE = 16 / EB;   // elements per 16-byte chunk = pairs per rotary lane
-    // Token tile.  Workgroups are dealt to the XCDs round-robin; when the tile
-    // count divides evenly, renumber the tiles so that each XCD streams one
-    // contiguous range of tokens of the row group instead of every eighth tile.
-    uint32_t tile = blockIdx.x;
-    if (g.xcd_tiles) tile = (tile % kXcds) * g.xcd_tiles + tile / kXcds;
     const int grp = blockIdx.y;
-
     const uint32_t tid = threadIdx.x;
     const uint32_t tl = g.lanes == 1 ? tid : __umulhi(tid, g.lanes_magic);   // tid / lanes, exact here
     const int lane = (int)(tid - tl * (uint32_t)g.lanes);
-    const int64_t t = (int64_t)tile * g.tok_per_block + tl;
+    const bool in_tile = (int)tl < g.tok_per_block;
 
-    // The prologue is straight-line and issues its loads in the order their
-    // results are needed: positions, then this lane's frequency, then the K/V
-    // rows.  Memory counters retire in order, so waiting for the positions and
-    // the frequency leaves the K/V loads in flight while the coefficients are
-    // formed.  Lanes and rows without work load from a clamped, in-range
-    // address and store nothing; they stay to the end because the wave shares
-    // its coefficients through shuffles.
-    int64_t src_slot, dst_slot = -1, delta = 0;
-    bool present = (int)tl < g.tok_per_block;   // a token of the chunk (or segment)
-    bool active;                                // ... whose source row can be read
-    int32_t dp = 0, spos = 0;
+    // Segment mode: the whole block works on one segment, whose delta is
+    // uniform; its tiles are shared out round-robin over the blocks of the
+    // x axis, which is sized for the longest segment (capped), so short
+    // segments leave few blocks idle.
+    SpliceSegment sg{};
+    int64_t n_tok = a.n_tokens;
     if constexpr (SEG) {
-        const SpliceSegment sg = a.segs[blockIdx.z];
-        src_slot = sg.src_slot0 + t;
-        present = present && t < sg.n_tokens;
-        active = present && src_slot >= 0 && src_slot < a.n_tokens;
-        const int64_t p = (int64_t)sg.dst_pos0 + t;
-        if (p >= 0 && p < sg.dst_seq_len) dst_slot = sg.dst_seq_base + p;
-        delta = (int64_t)sg.dst_pos0 - (int64_t)sg.src_pos0;
-        if (!active) src_slot = 0;
-    } else {
-        present = present && t < a.n_tokens;
-        active = present;
-        src_slot = active ? t : a.n_tokens - 1;
-        dp = a.dst_pos[src_slot];
-        spos = a.src_pos[src_slot];
+        sg = a.segs[blockIdx.z];
+        n_tok = sg.n_tokens;
     }
-    const double w_lane = om.w[__lane_id()];   // pair lane_id's frequency (used when n_pairs <= 64)
 
     // This lane's two chunks and whether they rotate.
     const bool is_k = lane < g.lanes_k;
@@ -262,105 +250,152 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Ome
         ca = m;
         cb = m + (g.n_vc >> 1);
     }
-
     const int64_t s0 = is_k ? a.src_k_stride[0] : a.src_v_stride[0];
     const int64_t s1 = is_k ? a.src_k_stride[1] : a.src_v_stride[1];
     const int64_t s2 = is_k ? a.src_k_stride[2] : a.src_v_stride[2];
     const int64_t d0 = is_k ? a.dst_k_stride[0] : a.dst_v_stride[0];
     const int64_t d1 = is_k ? a.dst_k_stride[1] : a.dst_v_stride[1];
-    const char* sbase = (is_k ? a.src_k : a.src_v) + src_slot * s2 * EB + ca * 16;
+    const int64_t d2 = is_k ? a.dst_k_stride[2] : a.dst_v_stride[2];
+    const char* const src_t = (is_k ? a.src_k : a.src_v) + ca * 16;
+    char* const dst_t = (is_k ? a.dst_k : a.dst_v) + ca * 16;
     const int ob = (cb - ca) * 16;
 
     // Rows r0..r1 of this block, walked as (layer, head) without division;
     // rows past r1 in the last unrolled step load row r1 - 1 again.
     const int r0 = grp * g.rows_per_block;
     const int r1 = min(r0 + g.rows_per_block, g.n_rows);
-    int layer = r0 / a.n_kv_heads;
-    int head = r0 - layer * a.n_kv_heads;
+    const int layer0 = r0 / a.n_kv_heads;
+    const int head0 = r0 - layer0 * a.n_kv_heads;
     const int last_layer = (r1 - 1) / a.n_kv_heads;
     const int last_head = (r1 - 1) - last_layer * a.n_kv_heads;
 
-    u32x4 va[kUnroll], vb[kUnroll];
-    int64_t doff[kUnroll];
-    auto load_rows = [&](int r) __attribute__((always_inline)) {
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            const bool in = r + u < r1;
-            const int l = in ? layer : last_layer, h = in ? head : last_head;
-            doff[u] = ((int64_t)l * d0 + (int64_t)h * d1) * EB;
-            const char* sp = sbase + ((int64_t)l * s0 + (int64_t)h * s1) * EB;
-            va[u] = ld16(sp);
-            vb[u] = ld16(sp + ob);
-            if (++head == a.n_kv_heads) {
-                head = 0;
-                ++layer;
-            }
-        }
-    };
-    load_rows(r0);
-
-    if constexpr (!SEG) {
-        dst_slot = dp;
-        delta = (int64_t)dp - (int64_t)spos;
-    }
-    const bool valid = dst_slot >= 0 && dst_slot < a.dst_capacity;
-    const bool work = active && valid;
-
-    // Rotation coefficients.  When every working lane of the wave has the same
-    // delta (always so in segment mode; so for a contiguous chunk in token
-    // mode), lane j evaluates pair j once and rotary lanes gather theirs by
-    // shuffle; otherwise each rotary lane evaluates its own CE pairs.
     float cs[CE], sn[CE];
-    const int32_t d_ref = __shfl((int32_t)delta, 0);
-    const bool uniform = __all(!work || delta == (int64_t)d_ref) && g.n_pairs <= kWave;
-    if (uniform) {
-        if (d_ref != 0) {
-            float c1 = 1.0f, s1v = 0.0f;
-            if (__lane_id() < g.n_pairs) delta_sincos(d_ref, w_lane, c1, s1v);
-#pragma unroll
-            for (int e = 0; e < CE; ++e) {
-                const int src = rope ? lane_pair<CE, STYLE>(lane, e, half_r) : 0;
-                cs[e] = __shfl(c1, src);
-                sn[e] = __shfl(s1v, src);
-            }
-        }
-        rope = rope && d_ref != 0;
-    } else {
-        rope = rope && delta != 0;
-        if (rope) {
-#pragma unroll
-            for (int e = 0; e < CE; ++e)
-                delta_sincos(delta, om.w[lane_pair<CE, STYLE>(lane, e, half_r)], cs[e], sn[e]);
-        }
-    }
+    bool have_coef = false;
 
-    if (work) {
-        char* dbase = (is_k ? a.dst_k : a.dst_v) +
-                      dst_slot * (is_k ? a.dst_k_stride[2] : a.dst_v_stride[2]) * EB + ca * 16;
-        for (int r = r0;;) {
+    for (uint32_t step = 0;; ++step) {
+        // Token tile.  Single chunk: one tile per block; workgroups are dealt to
+        // the XCDs round-robin, so when the tile count divides evenly the tiles
+        // are renumbered to give each XCD one contiguous range of tokens.
+        uint32_t tile;
+        if constexpr (SEG) {
+            tile = blockIdx.x + step * gridDim.x;
+            if ((int64_t)tile * g.tok_per_block >= n_tok) break;   // uniform over the block
+        } else {
+            tile = blockIdx.x;
+            if (g.xcd_tiles) tile = (tile % kXcds) * g.xcd_tiles + tile / kXcds;
+        }
+        const int64_t t = (int64_t)tile * g.tok_per_block + tl;
+
+        // Loads go out in the order their results are needed: positions, then
+        // the K/V rows.  Memory counters retire in order, so waiting for the
+        // positions (and, on the first tile, the frequency) leaves the K/V
+        // loads in flight while the coefficients are formed.  Lanes and rows
+        // without work load from a clamped, in-range address and store
+        // nothing; they stay to the end because the wave shares its
+        // coefficients through shuffles.
+        int64_t src_slot, dst_slot = -1, delta = 0;
+        const bool present = in_tile && t < n_tok;   // a token of the chunk (or segment)
+        bool active;                                 // ... whose source row can be read
+        int32_t dp = 0, spos = 0;
+        if constexpr (SEG) {
+            src_slot = sg.src_slot0 + t;
+            active = present && src_slot >= 0 && src_slot < a.n_tokens;
+            const int64_t p = (int64_t)sg.dst_pos0 + t;
+            if (p >= 0 && p < sg.dst_seq_len) dst_slot = sg.dst_seq_base + p;
+            delta = (int64_t)sg.dst_pos0 - (int64_t)sg.src_pos0;
+            if (!active) src_slot = 0;
+        } else {
+            active = present;
+            src_slot = active ? t : a.n_tokens - 1;
+            dp = a.dst_pos[src_slot];
+            spos = a.src_pos[src_slot];
+        }
+        const char* sbase = src_t + src_slot * s2 * EB;
+
+        int layer = layer0, head = head0;
+        u32x4 va[kUnroll], vb[kUnroll];
+        int64_t doff[kUnroll];
+        auto load_rows = [&](int r) __attribute__((always_inline)) {
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
-                if (r + u < r1) {
-                    if (rope) rotate_chunks<EB, STYLE>(va[u], vb[u], cs, sn);
-                    st16(dbase + doff[u], va[u]);
-                    st16(dbase + doff[u] + ob, vb[u]);
+                const bool in = r + u < r1;
+                const int l = in ? layer : last_layer, h = in ? head : last_head;
+                doff[u] = ((int64_t)l * d0 + (int64_t)h * d1) * EB;
+                const char* sp = sbase + ((int64_t)l * s0 + (int64_t)h * s1) * EB;
+                va[u] = ld16(sp);
+                vb[u] = ld16(sp + ob);
+                if (++head == a.n_kv_heads) {
+                    head = 0;
+                    ++layer;
                 }
             }
-            r += kUnroll;
-            if (r >= r1) break;
-            load_rows(r);
+        };
+        load_rows(r0);
+
+        if constexpr (!SEG) {
+            dst_slot = dp;
+            delta = (int64_t)dp - (int64_t)spos;
         }
+        const bool valid = dst_slot >= 0 && dst_slot < a.dst_capacity;
+        const bool work = active && valid;
+
+        // Rotation coefficients.  When every working lane of the wave has the
+        // same delta (always so in segment mode; so for a contiguous chunk in
+        // token mode), lane j evaluates pair j once and rotary lanes gather
+        // theirs by shuffle; otherwise each rotary lane evaluates its own CE
+        // pairs.  Segment mode forms them once per block.
+        bool rot = rope;
+        if (!SEG || !have_coef) {
+            const int32_t d_ref = __shfl((int32_t)delta, 0);
+            const bool uniform = __all(!work || delta == (int64_t)d_ref) && g.n_pairs <= kWave;
+            if (uniform) {
+                if (d_ref != 0) {
+                    float c1 = 1.0f, s1v = 0.0f;
+                    const int j = __lane_id();
+                    if (j < g.n_pairs) delta_sincos(d_ref, pair_omega(j, g), c1, s1v);
+#pragma unroll
+                    for (int e = 0; e < CE; ++e) {
+                        const int src = rope ? lane_pair<CE, STYLE>(lane, e, half_r) : 0;
+                        cs[e] = __shfl(c1, src);
+                        sn[e] = __shfl(s1v, src);
+                    }
+                }
+            } else if (rope && delta != 0) {
+#pragma unroll
+                for (int e = 0; e < CE; ++e)
+                    delta_sincos(delta, pair_omega(lane_pair<CE, STYLE>(lane, e, half_r), g), cs[e], sn[e]);
+            }
+            have_coef = true;
+        }
+        rot = rope && delta != 0;
+
+        if (work) {
+            char* dbase = dst_t + dst_slot * d2 * EB;
+            for (int r = r0;;) {
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) {
+                    if (r + u < r1) {
+                        if (rot) rotate_chunks<EB, STYLE>(va[u], vb[u], cs, sn);
+                        st16(dbase + doff[u], va[u]);
+                        st16(dbase + doff[u] + ob, vb[u]);
+                    }
+                }
+                r += kUnroll;
+                if (r >= r1) break;
+                load_rows(r);
+            }
+        }
+        if (present && !work && lane == 0 && grp == 0 && a.err_flag) atomicOr(a.err_flag, 1);
+        if constexpr (!SEG) break;
     }
-    if (present && !work && lane == 0 && grp == 0 && a.err_flag) atomicOr(a.err_flag, 1);
 }
 
 template <int EB, int STYLE>
-hipError_t launch_typed(const SpliceArgs& a, const Geo& g, const OmegaTable& om, dim3 grid, dim3 block,
-                        hipStream_t st) {
+hipError_t launch_typed(const SpliceArgs& a, const Geo& g, dim3 grid, dim3 block, hipStream_t st) {
     if (a.segs)
-        hipLaunchKernelGGL((splice_kernel<EB, STYLE, true>), grid, block, 0, st, a, g, om);
+        hipLaunchKernelGGL((splice_kernel<EB, STYLE, true>), grid, block, 0, st, a, g);
     else
-        hipLaunchKernelGGL((splice_kernel<EB, STYLE, false>), grid, block, 0, st, a, g, om);
+        hipLaunchKernelGGL((splice_kernel<EB, STYLE, false>), grid, block, 0, st, a, g);
     return hipGetLastError();
 }
 
@@ -389,26 +424,26 @@ hipError_t launch_splice(const SpliceArgs& a, hipStream_t stream) {
     const int64_t nz = seg ? a.n_segs : 1;
     if (tokens <= 0 || nz <= 0 || g.n_rows <= 0) return hipSuccess;
 
-    if (g.n_pairs > kOmegaPairs) return hipErrorInvalidValue;
+    if (g.n_pairs > (1 << kPairBits)) return hipErrorInvalidValue;
     g.rows_per_block = g.n_rows < kRowsPerBlock ? g.n_rows : kRowsPerBlock;
-    const int64_t n_tiles = (tokens + g.tok_per_block - 1) / g.tok_per_block;
+    int64_t n_tiles = (tokens + g.tok_per_block - 1) / g.tok_per_block;
+    if (seg && n_tiles > kSegTiles) n_tiles = kSegTiles;   // blocks loop over a segment's tiles
     const int64_t n_groups = (g.n_rows + g.rows_per_block - 1) / g.rows_per_block;
     if (n_tiles > 0x7fffffff || n_groups > 65535 || nz > 65535) return hipErrorInvalidConfiguration;
-    g.xcd_tiles = n_tiles % kXcds == 0 ? (int)(n_tiles / kXcds) : 0;
+    // Segment mode sizes the tile axis for the longest segment, so a shorter
+    // segment's tiles would all fall on the first XCDs: keep round-robin order.
+    g.xcd_tiles = !seg && n_tiles % kXcds == 0 ? (int)(n_tiles / kXcds) : 0;
     g.lanes_magic = g.lanes > 1 ? (uint32_t)((0x100000000ull + g.lanes - 1) / g.lanes) : 0;   // ceil(2^32/lanes)
 
-    OmegaTable om;
-    const int n_pairs = a.rope_dim / 2;
-    for (int i = 0; i < kOmegaPairs; ++i)
-        om.w[i] = i < n_pairs ? pow(a.theta, -2.0 * (double)i / (double)a.rope_dim) : 0.0;
+    for (int b = 0; b < kPairBits; ++b) g.rho[b] = pow(a.theta, -2.0 * (double)(1 << b) / (double)a.rope_dim);
 
     dim3 grid((unsigned)n_tiles, (unsigned)n_groups, (unsigned)nz);
     dim3 block((unsigned)kBlock);
     if (a.elem_bytes == 2)
-        return a.rope_style == kHalf ? launch_typed<2, 0>(a, g, om, grid, block, stream)
-                                     : launch_typed<2, 1>(a, g, om, grid, block, stream);
-    return a.rope_style == kHalf ? launch_typed<4, 0>(a, g, om, grid, block, stream)
-                                 : launch_typed<4, 1>(a, g, om, grid, block, stream);
+        return a.rope_style == kHalf ? launch_typed<2, 0>(a, g, grid, block, stream)
+                                     : launch_typed<2, 1>(a, g, grid, block, stream);
+    return a.rope_style == kHalf ? launch_typed<4, 0>(a, g, grid, block, stream)
+                                 : launch_typed<4, 1>(a, g, grid, block, stream);
 }
 
 }  // namespace pkv

@@ -245,6 +245,39 @@ def batched_case(bw: BatchedWorkload, plan, seed: int = 0, device="cpu", layers:
     return out
 
 
+def batched_segments(plan):
+    """Segment records (pkv_segment fields) of the batched composition: one per
+    (sequence, skill), in sequence order."""
+    segs = []
+    for sq in plan["seqs"]:
+        for sg in sq["segs"]:
+            segs.append(dict(src_slot0=sg["src_slot0"], dst_seq_base=sq["seq_base"], n_tokens=sg["n_tokens"],
+                             src_pos0=sg["src_pos0"], dst_pos0=sg["dst_pos0"], dst_seq_len=sq["kv_len"]))
+    return segs
+
+
+def batched_splice_bytes(bw: BatchedWorkload, plan) -> int:
+    """Algorithmic bytes of the batched splice: every spliced token's K and V rows read once and written once."""
+    tokens = sum(sg["n_tokens"] for sq in plan["seqs"] for sg in sq["segs"])
+    return 2 * 2 * tokens * bw.n_layers * bw.n_kv_heads * bw.head_dim * 2
+
+
+def batched_attn_flops(bw: BatchedWorkload, plan) -> int:
+    """Algorithmic flops of the ragged suffix attention: 4*d per (query, head, visible key)."""
+    vis = 0
+    for sq in plan["seqs"]:
+        C = sq["ctx"]
+        vis += sum(min(sq["kv_len"], C + i + 1) for i in range(bw.n_q))
+    return 4 * bw.head_dim * bw.n_heads * vis * bw.n_layers
+
+
+def batched_attn_bytes(bw: BatchedWorkload, plan) -> int:
+    """Algorithmic bytes: each sequence's K/V over its kv_len read once per layer, Q read, O written."""
+    kv = sum(sq["kv_len"] for sq in plan["seqs"]) * bw.n_kv_heads * 2 * bw.head_dim
+    qo = bw.n_seqs * bw.n_q * bw.n_heads * 2 * bw.head_dim
+    return (kv + qo) * 2 * bw.n_layers
+
+
 def to_numpy_bits(t: torch.Tensor) -> np.ndarray:
     """Storage bits of a CPU tensor as numpy: bf16 -> uint16, fp32 -> float32."""
     t = t.detach().cpu().contiguous()
