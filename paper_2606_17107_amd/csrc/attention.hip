@@ -10,6 +10,9 @@
 #ifndef PKV_MLA_STAGES
 #define PKV_MLA_STAGES 2       // LDS pipeline depth of the MLA kernel
 #endif
+#ifndef PKV_MLA_WAVES
+#define PKV_MLA_WAVES 4        // waves per MLA workgroup (pairs share 32 rows)
+#endif
 
 namespace pkv {
 
@@ -153,9 +156,10 @@ Plan make_plan(const AttnArgs& a, int splits) {
     const int64_t m_rows = (int64_t)a.max_q * p.G;
     int tile = 64;
     if (a.variant == 1) {
-        // MLA: 4 waves = 2 blocks of 32 rows x 2 output halves; 32-key tiles.
+        // MLA: wave pairs share 32 rows (each pair: two score-channel halves
+        // and two output halves); 32-key tiles.
         p.qb = 1;
-        p.nw = 4;
+        p.nw = PKV_MLA_WAVES;
         p.ns = PKV_MLA_STAGES;
         tile = 32;
     } else {
@@ -166,7 +170,7 @@ Plan make_plan(const AttnArgs& a, int splits) {
         p.ns = PKV_ATTN_SHAPE == 1 ? 4 : 2;
         tile = PKV_ATTN_SHAPE == 1 ? 32 : 64;
     }
-    p.BM = a.dtype == 1 ? 64 : (a.variant == 1 ? 64 : p.nw * 32 * p.qb);
+    p.BM = a.dtype == 1 ? 64 : (a.variant == 1 ? p.nw / 2 * 32 : p.nw * 32 * p.qb);
     p.rbs = (int)((m_rows + p.BM - 1) / p.BM);
     if (p.rbs < 1) p.rbs = 1;
     p.splits = splits;
@@ -229,7 +233,7 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
     const int64_t n_wg = groups_padded * p.rbs;
     if (n_wg <= 0) return hipSuccess;
     if (n_wg > 0x7fffffff) return hipErrorInvalidValue;
-    dim3 grid((unsigned)n_wg), block(256);
+    dim3 grid((unsigned)n_wg), block(256);   // the bf16 launchers set their own block size
     if (a.dtype == 1) {
         if (a.head_dim == 64)
             hipLaunchKernelGGL((attn_gqa_f32<64>), grid, block, 0, stream, a, p);

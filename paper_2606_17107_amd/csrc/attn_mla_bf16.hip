@@ -19,12 +19,18 @@
 //     ds_read_b64_tr_b16 (channels 0..511).
 //   * Tiles of 32 keys (36 KB) stream HBM -> LDS by LDS-DMA through NS
 //     stages; chunks XOR-swizzled by the key as in the GQA kernel.
+//   * Four waves (two pairs, 64 rows) per workgroup and two stages by
+//     default; eight waves (two per SIMD) and three stages are selectable at
+//     build time and measured no faster.
 #include <type_traits>
 
 #include "attn_common.h"
 
 #ifndef PKV_MLA_STAGES
 #define PKV_MLA_STAGES 2
+#endif
+#ifndef PKV_MLA_WAVES
+#define PKV_MLA_WAVES 4
 #endif
 
 namespace pkv {
@@ -35,16 +41,24 @@ constexpr int DQK = 576;       // score channels
 constexpr int DV = 512;        // value (latent) channels
 constexpr int MCH = DQK / 8;   // 16-byte chunks per row: 72
 
-__device__ inline int mswz(int key) { return ((key & 3) << 1) | ((key >> 2) & 1); }
+// XOR swizzle of the low three bits of a row's 16-byte chunk index by its key.
+// A row is 72 chunks, so consecutive keys start in alternate halves of the 16
+// bank groups (16 bytes each).  K operand reads take one chunk from each of 16
+// consecutive keys: for either key parity the swizzle is a bijection of
+// (key >> 1) & 7, so the 16 reads hit 16 groups.  Transposed V reads take a
+// 4-chunk aligned window from each of 4 consecutive keys: keys 4q and 4q+2
+// (and 4q+1, 4q+3) differ in bit 2 of the swizzle, which moves the window to
+// the other half of its 8-chunk group.
+__device__ inline int mswz(int key) { return (((key >> 1) & 1) << 2) | ((key >> 2) & 3); }
 
-template <int NS>
-__global__ __launch_bounds__(256) void attn_mla_bf16_kernel(AttnArgs a, Plan p) {
-    constexpr int NW = 4;
-    constexpr int PER = MBN * MCH / 64 / NW;   // LDS-DMA loads per wave per tile: 9
+template <int NS, int NW>
+__global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs a, Plan p) {
+    constexpr int NBLK = MBN * MCH / 64;       // 64-lane LDS-DMA blocks per tile: 36
+    constexpr int PER = (NBLK + NW - 1) / NW;  // blocks of the busiest wave per tile
     constexpr int KS = DQK / 16 / 2;           // k-steps per wave (its half of the channels): 18
     constexpr int DB = DV / 64;                // 32-channel blocks per wave (its half of DV): 8
     constexpr int TE = MBN * DQK;              // elements per tile
-    static_assert(MBN * MCH % (64 * NW) == 0, "tile loads must split evenly over the waves");
+    static_assert(NW == 4 || NW == 8, "four or eight waves (pairs of waves share 32 rows)");
     static_assert(NS >= 2 && NS <= 4, "2..4 stages");
 
     __shared__ __attribute__((aligned(16))) uint16_t t0_[TE], t1_[TE], t2_[NS > 2 ? TE : 8], t3_[NS > 3 ? TE : 8];
@@ -82,7 +96,9 @@ __global__ __launch_bounds__(256) void attn_mla_bf16_kernel(AttnArgs a, Plan p) 
     const int wmax = wave_max_i(row_end);
     if (lane == 0) red[wave] = wmax;
     __syncthreads();
-    const int e_max = max(max(red[0], red[1]), max(red[2], red[3]));
+    int e_max = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) e_max = max(e_max, red[w]);
     const int k_begin = split * p.chunk;
     const int loop_end = min(min(si.kvl, k_begin + p.chunk), e_max);
     const int n_tiles = loop_end > k_begin ? (loop_end - k_begin + MBN - 1) / MBN : 0;
@@ -102,29 +118,64 @@ __global__ __launch_bounds__(256) void attn_mla_bf16_kernel(AttnArgs a, Plan p) 
     const uint16_t* kbase = (const uint16_t*)a.k + (int64_t)layer * a.k_stride[0] + si.base * a.k_stride[2];
     const int64_t kss = a.k_stride[2];
     const int last_key = loop_end - 1;
+    // Wave w moves blocks w, w + NW, ... of each tile (NBLK / NW or one more):
+    // lane l of block b fills LDS chunk slot 64b + l (key slot / 72, physical
+    // chunk slot % 72, holding logical chunk phys ^ mswz(key)).
+    const int n_mine = (NBLK - wave + NW - 1) / NW;   // wave-uniform
     int32_t src_off[PER];
     int key_of[PER];
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-        const int slot = (wave * PER + i) * 64 + lane;
+        const int b = i < n_mine ? wave + i * NW : wave;   // idle slots mirror block `wave` (never issued)
+        const int slot = b * 64 + lane;
         key_of[i] = slot / MCH;
         const int logical = (slot % MCH) ^ mswz(key_of[i]);
         src_off[i] = (int32_t)((int64_t)key_of[i] * kss * 2 + logical * 16);
     }
     auto issue = [&](int t0, uint16_t* dst_stage) {
         const char* kt = (const char*)(kbase + (int64_t)t0 * kss);
-        const uint32_t lds0 = lds_addr_of(dst_stage + wave * PER * 64 * 8);
-        if (t0 + MBN <= loop_end) {
+        const uint32_t lds0 = lds_addr_of(dst_stage + wave * 64 * 8);
+        const bool full = t0 + MBN <= loop_end;
 #pragma unroll
-            for (int i = 0; i < PER; ++i) lds_dma16(lds0 + i * 1024, kt, (uint32_t)src_off[i]);
-        } else {
-#pragma unroll
-            for (int i = 0; i < PER; ++i) {
+        for (int i = 0; i < PER; ++i) {
+            if (i < n_mine) {
                 const int over = t0 + key_of[i] - last_key;
-                lds_dma16(lds0 + i * 1024, kt, (uint32_t)(src_off[i] - (over > 0 ? over * (int32_t)(kss * 2) : 0)));
+                const uint32_t back = !full && over > 0 ? (uint32_t)(over * (int32_t)(kss * 2)) : 0u;
+                lds_dma16(lds0 + i * NW * 1024, kt, (uint32_t)src_off[i] - back);
             }
         }
     };
+
+    // Per-lane LDS element offsets of the MFMA operands within a stage.  The
+    // swizzle only permutes the low three bits of a chunk index, so:
+    //   K (A of S^T = K Q^T), k-step ks: logical chunk c0 + 2ks of key j
+    //     (c0 = 36 vhalf + hl) sits at kofs[ks & 3] + (ks >> 2) * 64;
+    //   V^T (A of O^T = V^T P^T), 16-key step st, half b, channel block db:
+    //     lane group g = lane >> 4 reads channels 256 vhalf + 32db + 16(g&1) +
+    //     4(sl&3)..+3 of key 16st + 8b + 4(g>>1) + (sl>>2), sl = lane & 15 (the
+    //     key order of the P^T accumulator); the swizzle of that key depends
+    //     only on its low four bits, so the read is at
+    //     vofs[db & 1][b] + 16st * 576 + (db >> 1) * 64.
+    int kofs[4], vofs[2][2];
+    {
+        const int sk = mswz(j);
+        const int c0 = vhalf * KS * 2 + hl;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int c = c0 + 2 * q;
+            kofs[q] = j * DQK + ((c & ~7) | ((c & 7) ^ sk)) * 8;
+        }
+        const int g = lane >> 4, sl = lane & 15;
+        const int vkey = (g >> 1) * 4 + (sl >> 2);
+#pragma unroll
+        for (int par = 0; par < 2; ++par)
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                const int key = b * 8 + vkey;
+                const int c7 = par * 4 + (g & 1) * 2 + ((sl & 3) >> 1);
+                vofs[par][b] = key * DQK + (vhalf * 32 + (c7 ^ mswz(key))) * 8 + (sl & 1) * 4;
+            }
+    }
 
     f32x16 o[DB];
 #pragma unroll
@@ -135,21 +186,16 @@ __global__ __launch_bounds__(256) void attn_mla_bf16_kernel(AttnArgs a, Plan p) 
 
     auto compute = [&](int t0, const uint16_t* ts, auto mask_tag) {
         constexpr bool MASK = decltype(mask_tag)::value;
-        // Partial S^T = K Q^T over this wave's 288 channels, 32 keys, in two
-        // independent accumulation chains.
-        f32x16 sa = f32x16{}, sb = f32x16{};
-        const int key = j;
+        // Partial S^T = K Q^T over this wave's 288 channels, 32 keys (one
+        // accumulation chain: dependent MFMAs on the same accumulator issue
+        // back to back).
+        f32x16 s = f32x16{};
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-            const int phys = ((vhalf * KS + ks) * 2 + hl) ^ mswz(key);
-            const u32x4 kv = *(const u32x4*)(ts + key * DQK + phys * 8);
-            if (ks & 1)
-                sb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kv), qf[ks], sb, 0, 0, 0);
-            else
-                sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kv), qf[ks], sa, 0, 0, 0);
+            const u32x4 kv = *(const u32x4*)(ts + kofs[ks & 3] + (ks >> 2) * 64);
+            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kv), qf[ks], s, 0, 0, 0);
         }
         sched_reads_mfma<KS, 1, 1>();
-        f32x16 s = sa + sb;
         // Exchange the partial scores with the other wave of the pair (the
         // lanes of both waves hold the same (key, row) elements).
         float* mine = xch + wave * 1024;
@@ -218,21 +264,15 @@ __global__ __launch_bounds__(256) void attn_mla_bf16_kernel(AttnArgs a, Plan p) 
             pb[st] = __builtin_convertvector(pv, bf16x8);
         }
         // O^T += V^T P^T: V is channels 0..511 of the same tile.
-        const int g = lane >> 4, sl = lane & 15;
-        const int hh = g >> 1;
 #pragma unroll
         for (int st = 0; st < 2; ++st) {
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
                 s16x4 part[2];
 #pragma unroll
-                for (int b = 0; b < 2; ++b) {
-                    const int kk = st * 16 + b * 8 + hh * 4 + (sl >> 2);
-                    const int col = vhalf * 256 + db * 32 + (g & 1) * 16 + (sl & 3) * 4;
-                    const int phys = (col >> 3) ^ mswz(kk);
+                for (int b = 0; b < 2; ++b)
                     part[b] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                        PKV_LDS(s16x4, ts + kk * DQK + phys * 8 + (col & 7)));
-                }
+                        PKV_LDS(s16x4, ts + vofs[db & 1][b] + st * 16 * DQK + (db >> 1) * 64));
                 const s16x4 p0 = part[0], p1 = part[1];
                 const bf16x8 vf = __builtin_bit_cast(
                     bf16x8, (short __attribute__((ext_vector_type(8)))){p0[0], p0[1], p0[2], p0[3], p1[0], p1[1],
@@ -243,11 +283,17 @@ __global__ __launch_bounds__(256) void attn_mla_bf16_kernel(AttnArgs a, Plan p) 
         sched_reads_mfma<2 * DB, 2, 1>();
     };
 
-    auto wait_outstanding = [&](int tiles_after) {
-        if (NS > 3 && tiles_after >= 3) wait_vmcnt<(NS > 3 ? 3 : 1) * PER>();
-        else if (NS > 2 && tiles_after >= 2) wait_vmcnt<(NS > 2 ? 2 : 1) * PER>();
-        else if (tiles_after == 1) wait_vmcnt<PER>();
+    // Each wave waits for its own loads: n_mine per tile (PER or PER - 1).
+    auto wait_tiles = [&](int tiles_after, auto per_tag) {
+        constexpr int Q = decltype(per_tag)::value;
+        if (NS > 3 && tiles_after >= 3) wait_vmcnt<(NS > 3 ? 3 : 1) * Q>();
+        else if (NS > 2 && tiles_after >= 2) wait_vmcnt<(NS > 2 ? 2 : 1) * Q>();
+        else if (tiles_after == 1) wait_vmcnt<Q>();
         else wait_vmcnt<0>();
+    };
+    auto wait_outstanding = [&](int tiles_after) {
+        if (n_mine == PER) wait_tiles(tiles_after, std::integral_constant<int, PER>{});
+        else wait_tiles(tiles_after, std::integral_constant<int, (PER > 1 ? PER - 1 : 1)>{});
     };
 #pragma unroll
     for (int s = 0; s < NS - 1; ++s)
@@ -313,7 +359,9 @@ __global__ __launch_bounds__(256) void attn_mla_bf16_kernel(AttnArgs a, Plan p) 
 }  // namespace
 
 hipError_t launch_attn_mla_bf16(const AttnArgs& a, const Plan& p, dim3 grid, hipStream_t stream) {
-    hipLaunchKernelGGL((attn_mla_bf16_kernel<PKV_MLA_STAGES>), grid, dim3(256), 0, stream, a, p);
+    if (p.nw != PKV_MLA_WAVES || p.ns != PKV_MLA_STAGES || p.BM != PKV_MLA_WAVES / 2 * 32) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((attn_mla_bf16_kernel<PKV_MLA_STAGES, PKV_MLA_WAVES>), grid, dim3(PKV_MLA_WAVES * 64), 0, stream,
+                       a, p);
     return hipGetLastError();
 }
 
