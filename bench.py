@@ -41,8 +41,9 @@ def log(*a):
 class GqaStep:
     """Inputs and launches of one workload (single sequence, GQA or MLA)."""
 
-    def __init__(self, w: synth.Workload, n_splits: int, seed: int = 0):
+    def __init__(self, w: synth.Workload, n_splits: int, seed: int = 0, window: int = 0):
         self.w = w
+        self.window = window
         dev = torch.device("cuda")
         c = synth.gqa_case(w, seed=seed, device=dev)
         self.cache_k = c["ctx_k"]
@@ -75,7 +76,7 @@ class GqaStep:
                                              w.rope_offset, w.rope_style)
         variant = pkv.PKV_ATTN_MLA if w.mla else pkv.PKV_ATTN_GQA
         self.desc = pkv.make_attn_desc(self.q, self.cache_k, self.v_view, self.out, w.kv_len, variant=variant,
-                                       n_splits=n_splits)
+                                       n_splits=n_splits, window=window)
         self.ws_bytes = pkv.pkv_attention_workspace_size(self.desc, w.n_heads, w.n_kv_heads, w.head_dim)
         self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device=dev)
         torch.cuda.synchronize()
@@ -100,15 +101,15 @@ class GqaStep:
 
     def describe(self):
         w = self.w
-        return ("%s: %d layers, %d/%d heads, d %d, %d-token skill %d->%d, %d-token suffix over %d slots"
+        return ("%s: %d layers, %d/%d heads, d %d, %d-token skill %d->%d, %d-token suffix over %d slots%s"
                 % (w.name, w.n_layers, w.n_heads, w.n_kv_heads, w.head_dim, w.skill_tokens, w.src_pos0, w.dst_pos0,
-                   w.n_q, w.kv_len))
+                   w.n_q, w.kv_len, ", sliding window %d" % self.window if self.window else ""))
 
     def attn_flops(self):
-        return self.w.attn_flops()
+        return self.w.attn_flops(self.window)
 
     def attn_bytes(self):
-        return self.w.attn_bytes()
+        return self.w.attn_bytes(self.window)
 
 
 class BatchedStep:
@@ -383,6 +384,8 @@ def main():
                     help="keep warming up until this much wall time has passed (clock ramp)")
     ap.add_argument("--workload", default="gqa8b", choices=sorted(synth.WORKLOADS) + ["batched"])
     ap.add_argument("--splits", type=int, default=0, help="KV splits for attention (0 = library choice)")
+    ap.add_argument("--window", type=int, default=0,
+                    help="sliding-window attention over the full cache (0 = causal; single-sequence workloads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -405,7 +408,7 @@ def main():
         step = BatchedStep(w, args.splits)
     else:
         w = synth.WORKLOADS[args.workload]
-        step = GqaStep(w, args.splits)
+        step = GqaStep(w, args.splits, window=args.window)
     log("workload", w)
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream

@@ -180,7 +180,9 @@ typedef struct pkv_attn_desc {
     int32_t max_q;          /* >= the largest per-sequence query count */
     int32_t max_kv_len;     /* >= every kv_len[s]; larger values are clamped to it */
     int32_t n_splits;       /* KV-length splits; 0 = the library chooses */
-    int32_t reserved;       /* must be 0 */
+    int32_t window;         /* 0: full causal attention.  W > 0: sliding window, slot j is visible
+                               only if j > q_pos - W as well (the full cache is kept and the mask
+                               enforces the window; Sec. 8 sliding-window configuration fix) */
     const int32_t* cu_q;    /* device int32 [n_seqs+1]; NULL allowed when n_seqs == 1 */
     const int64_t* kv_base; /* device int64 [n_seqs]; NULL = every sequence starts at slot 0 */
     int64_t cache_slots;    /* slots present in k_cache/v_cache; reads past it are masked out */
@@ -202,7 +204,7 @@ size_t pkv_attention_workspace_size(const pkv_attn_desc* desc, int32_t n_q_heads
  * (Sec. 5 "Linear-time TTFT"; Sec. 4 erratum; Sec. 6 delta prefill).  For layer
  * l, query row i of sequence s and query head h (KV head g = h / (n_q_heads /
  * n_kv_heads)):
- *     visible j: 0 <= j < kv_len[s], j <= q_pos[i]
+ *     visible j: 0 <= j < kv_len[s], j <= q_pos[i], and j > q_pos[i] - window if window > 0
  *     out[l][i][h] = sum_j softmax_j(scale * <q[l][i][h], k[l][g][kv_base[s]+j]>) v[l][g][kv_base[s]+j]
  * q is post-RoPE (q_pos only masks).  bf16: QK^T and PV on bf16 MFMA with fp32
  * accumulation, softmax statistics in fp32, probabilities rounded to bf16
@@ -212,7 +214,7 @@ size_t pkv_attention_workspace_size(const pkv_attn_desc* desc, int32_t n_q_heads
  * pkv_attention_workspace_size() bytes (may be NULL when that is 0), owned by
  * the caller, contents scratch.
  * Errors: PKV_ERR_NULL, PKV_ERR_SHAPE (n_q_heads % n_kv_heads != 0, sizes <= 0,
- * workspace too small, MLA shape not 576/512 with one KV head or v_cache not
+ * window < 0, workspace too small, MLA shape not 576/512 with one KV head or v_cache not
  * k_cache), PKV_ERR_ALIGN,
  * PKV_ERR_UNSUPPORTED (head_dim other than 64 or 128 for GQA; fp32 MLA),
  * PKV_ERR_DEVICE. */

@@ -65,7 +65,7 @@ def _load():
     lib.pkvref_attention.restype = None
     lib.pkvref_attention.argtypes = [
         ctypes.c_int, P, P, P, P, P, P, i64, i64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-        ctypes.c_int, f64, i64, i64, i64, i64, i64, i64]
+        ctypes.c_int, f64, i64, i64, i64, i64, i64, i64, i64]
     lib.pkvref_max_threads.restype = ctypes.c_int
     lib.pkvref_set_threads.argtypes = [ctypes.c_int]
     _lib = lib
@@ -150,8 +150,9 @@ def reposition_splice(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, theta, rope_
         _ptr(dks), _ptr(dvs), cap))
 
 
-def attention(q, k, v, q_pos, kv_len, scale):
-    """Causal attention of one layer and one sequence, fp64.
+def attention(q, k, v, q_pos, kv_len, scale, window=0):
+    """Causal attention of one layer and one sequence, fp64 (``window`` > 0:
+    slot j is also required to satisfy j > q_pos - window).
 
     q ``[n_q][H][d_qk]``, k ``[Hkv][slots][d_qk]``, v ``[Hkv][slots][d_v]`` (v may be a
     view into k, e.g. the MLA latent).  Returns ``(out [n_q][H][d_v] fp64,
@@ -172,5 +173,5 @@ def attention(q, k, v, q_pos, kv_len, scale):
     lse = np.zeros((n_q, H), dtype=np.float64)
     _load().pkvref_attention(dt, _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(q_pos), n_q,
                              int(kv_len), H, Hkv, d_qk, d_v, float(scale), qs[0], qs[1], ks[0], ks[1],
-                             vs[0], vs[1])
+                             vs[0], vs[1], int(window))
     return out, lse

@@ -186,20 +186,27 @@ int64_t pkvref_reposition_splice(int dtype, const void* src_k, const void* src_v
  *   out: fp64, element (i, h, c) at out[(i*n_heads + h)*d_v + c]
  *   lse: fp64 [n_q*n_heads] (optional), natural-log sum-exp of scaled scores
  * Query head h reads KV head h / (n_heads / n_kv_heads).  Slot j is visible to
- * query i iff j < kv_len and j <= q_pos[i].  A row with no visible slot gets
- * out = 0 and lse = -inf. */
+ * query i iff j < kv_len and j <= q_pos[i], and, for window > 0, also
+ * j > q_pos[i] - window: the sliding-window layers keep the full per-token
+ * cache and the mask alone enforces the window (Sec. 8, the sliding-window
+ * configuration fix; Fig. "attention-variant adapters" (c)).  A row with no
+ * visible slot gets out = 0 and lse = -inf. */
 void pkvref_attention(int dtype, const void* q, const void* k, const void* v, double* out,
                       double* lse, const int32_t* q_pos, int64_t n_q, int64_t kv_len, int n_heads,
                       int n_kv_heads, int d_qk, int d_v, double scale, int64_t q_tok,
                       int64_t q_head, int64_t k_head, int64_t k_tok, int64_t v_head,
-                      int64_t v_tok) {
+                      int64_t v_tok, int64_t window) {
     int group = n_heads / n_kv_heads;
 #pragma omp parallel for collapse(2) schedule(dynamic, 1)
     for (int64_t i = 0; i < n_q; ++i) {
         for (int h = 0; h < n_heads; ++h) {
             int g = h / group;
-            int64_t n_vis = kv_len;
-            if ((int64_t)q_pos[i] + 1 < n_vis) n_vis = (int64_t)q_pos[i] + 1;
+            /* visible slots lo .. hi-1 */
+            int64_t hi = kv_len;
+            if ((int64_t)q_pos[i] + 1 < hi) hi = (int64_t)q_pos[i] + 1;
+            int64_t lo = 0;
+            if (window > 0 && (int64_t)q_pos[i] - window + 1 > lo) lo = (int64_t)q_pos[i] - window + 1;
+            int64_t n_vis = hi - lo;
             if (n_vis < 0) n_vis = 0;
             double* o = out + (i * n_heads + h) * d_v;
             for (int c = 0; c < d_v; ++c) o[c] = 0.0;
@@ -214,7 +221,7 @@ void pkvref_attention(int dtype, const void* q, const void* k, const void* v, do
                 double s = 0.0;
                 for (int c = 0; c < d_qk; ++c)
                     s += ref_load(q, dtype, i * q_tok + h * q_head + c) *
-                         ref_load(k, dtype, g * k_head + j * k_tok + c);
+                         ref_load(k, dtype, g * k_head + (lo + j) * k_tok + c);
                 sc[j] = s * scale;
                 if (sc[j] > m) m = sc[j];
             }
@@ -223,7 +230,7 @@ void pkvref_attention(int dtype, const void* q, const void* k, const void* v, do
             for (int64_t j = 0; j < n_vis; ++j) {
                 double w = exp(sc[j] - m);
                 sum += w;
-                for (int c = 0; c < d_v; ++c) o[c] += w * ref_load(v, dtype, g * v_head + j * v_tok + c);
+                for (int c = 0; c < d_v; ++c) o[c] += w * ref_load(v, dtype, g * v_head + (lo + j) * v_tok + c);
             }
             free(sc);
             for (int c = 0; c < d_v; ++c) o[c] /= sum;

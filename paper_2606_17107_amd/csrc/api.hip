@@ -162,7 +162,7 @@ pkv_status check_attention(const void* q, const void* k, const void* v, void* ou
     if (d->dtype != PKV_BF16 && d->dtype != PKV_F32) return fail(PKV_ERR_UNSUPPORTED, "dtype %d", d->dtype);
     if (d->variant != PKV_ATTN_GQA && d->variant != PKV_ATTN_MLA)
         return fail(PKV_ERR_UNSUPPORTED, "variant %d", d->variant);
-    if (d->reserved != 0) return fail(PKV_ERR_SHAPE, "desc.reserved must be 0");
+    if (d->window < 0) return fail(PKV_ERR_SHAPE, "desc.window (%d) must be >= 0", d->window);
     if (H <= 0 || Hkv <= 0 || D <= 0 || H % Hkv)
         return fail(PKV_ERR_SHAPE, "n_q_heads (%d) must be a positive multiple of n_kv_heads (%d)", H, Hkv);
     if (d->n_layers <= 0 || d->n_seqs <= 0 || d->total_q < 0 || d->max_q < 0 || d->max_kv_len < 0 ||
@@ -228,6 +228,7 @@ pkv_status check_attention(const void* q, const void* k, const void* v, void* ou
     a.max_q = d->cu_q ? d->max_q : d->total_q;
     a.max_kv_len = d->max_kv_len;
     a.n_splits = d->n_splits;
+    a.window = d->window;
     a.cache_slots = d->cache_slots;
     a.scale = scale;
     for (int i = 0; i < 3; ++i) {

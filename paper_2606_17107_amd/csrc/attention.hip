@@ -29,7 +29,7 @@ __global__ __launch_bounds__(256) void attn_gqa_f32(AttnArgs a, Plan p) {
     constexpr int DQ = D / 4;
     __shared__ float k_lds[BN * D];
     __shared__ float v_lds[BN * D];
-    __shared__ int red[4];
+    __shared__ int red[4], red_start[4];
 
     int group, rb;
     if (!decode(p, group, rb)) return;
@@ -51,10 +51,17 @@ __global__ __launch_bounds__(256) void attn_gqa_f32(AttnArgs a, Plan p) {
     const int head = kvh * p.G + (row_ok ? m - qi * p.G : 0);
     const int qpos = row_ok ? a.q_pos[si.q0 + qi] : -1;
     const int row_end = row_ok ? max(0, min(si.kvl, qpos + 1)) : 0;
+    const int row_start = a.window > 0 && row_ok ? max(0, qpos - a.window + 1) : 0;   // sliding window
     const int wmax = wave_max_i(row_end);
-    if ((tid & 63) == 0) red[tid >> 6] = wmax;
+    const int wsmin = wave_min_i(row_ok ? row_start : 0x7fffffff);
+    if ((tid & 63) == 0) {
+        red[tid >> 6] = wmax;
+        red_start[tid >> 6] = wsmin;
+    }
     __syncthreads();
     const int loop_end = max(max(red[0], red[1]), max(red[2], red[3]));
+    const int s_min = min(min(red_start[0], red_start[1]), min(red_start[2], red_start[3]));
+    const int k_first = s_min == 0x7fffffff ? 0 : s_min / BN * BN;   // tiles before every window are skipped
 
     const float* qrow = (const float*)a.q + (int64_t)layer * a.q_stride[0] +
                         (int64_t)(si.q0 + qi) * a.q_stride[1] + (int64_t)head * a.q_stride[2] + part * DQ;
@@ -69,7 +76,7 @@ __global__ __launch_bounds__(256) void attn_gqa_f32(AttnArgs a, Plan p) {
                          si.base * a.k_stride[2];
     const float* vbase = (const float*)a.v + (int64_t)layer * a.v_stride[0] + (int64_t)kvh * a.v_stride[1] +
                          si.base * a.v_stride[2];
-    for (int t0 = 0; t0 < loop_end; t0 += BN) {
+    for (int t0 = k_first; t0 < loop_end; t0 += BN) {
         __syncthreads();
         for (int id = tid; id < BN * D / 4; id += 256) {
             const int key = id / (D / 4), c = id % (D / 4);
@@ -89,7 +96,7 @@ __global__ __launch_bounds__(256) void attn_gqa_f32(AttnArgs a, Plan p) {
             for (int c = 0; c < DQ; ++c) s = fmaf(qv[c], k_lds[kk * D + part * DQ + c], s);
             s += __shfl_xor(s, 1);
             s += __shfl_xor(s, 2);
-            if (t0 + kk >= row_end) continue;   // invisible to this row (uniform over its 4 lanes)
+            if (t0 + kk >= row_end || t0 + kk < row_start) continue;   // invisible to this row (uniform over its 4 lanes)
             const float m_new = fmaxf(m_run, s);
             const float alpha = expf(m_run - m_new);
             const float pe = expf(s - m_new);

@@ -74,7 +74,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
     // operand serves every stage through the 16-bit immediate offset of the
     // LDS read (K stages within 48 KB of the block, V stages of the V half).
     __shared__ __attribute__((aligned(16))) uint16_t stage_lds[2 * NS * TE];
-    __shared__ int red[NW], red_min[NW];
+    __shared__ int red[NW], red_min[NW], red_start[NW];
     auto kst = [&](int st) -> uint16_t* __attribute__((always_inline)) { return stage_lds + st * TE; };
     auto vst = [&](int st) -> uint16_t* __attribute__((always_inline)) { return stage_lds + (NS + st) * TE; };
 
@@ -97,10 +97,12 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
     const int j = lane & 31;
     const int hl = lane >> 5;
 
-    // Rows of this lane (one per 32-row block) and their visible key ranges.
-    int qi[QB], head[QB], row_end[QB];
+    // Rows of this lane (one per 32-row block) and their visible key ranges
+    // [row_start, row_end): causal, and with a sliding window also
+    // row_start = q_pos - window + 1.
+    int qi[QB], head[QB], row_end[QB], row_start[QB];
     bool row_ok[QB];
-    int rmax = 0, rmin = 0x7fffffff;
+    int rmax = 0, rmin = 0x7fffffff, smin = 0x7fffffff, smax = 0;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
         const int m = m0 + (wave * QB + qb) * 32 + j;
@@ -109,25 +111,36 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
         head[qb] = kvh * p.G + (row_ok[qb] ? m - qi[qb] * p.G : 0);
         const int qpos = row_ok[qb] ? a.q_pos[si.q0 + qi[qb]] : -1;
         row_end[qb] = row_ok[qb] ? max(0, min(si.kvl, qpos + 1)) : 0;
+        row_start[qb] = a.window > 0 && row_ok[qb] ? max(0, qpos - a.window + 1) : 0;
         rmax = max(rmax, row_end[qb]);
-        if (row_ok[qb]) rmin = min(rmin, row_end[qb]);
+        if (row_ok[qb]) {
+            rmin = min(rmin, row_end[qb]);
+            smin = min(smin, row_start[qb]);
+            smax = max(smax, row_start[qb]);
+        }
     }
     const int wmin = wave_min_i(rmin);
     const int wmax = wave_max_i(rmax);
+    const int wsmin = wave_min_i(smin);
+    const int wsmax = wave_max_i(smax);   // tiles below this need the window mask
     if (lane == 0) {
         red[wave] = wmax;
         red_min[wave] = wmin;
+        red_start[wave] = wsmin;
     }
     __syncthreads();
-    int e_max = 0, e_min = 0x7fffffff;
+    int e_max = 0, e_min = 0x7fffffff, s_min = 0x7fffffff;
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
         e_max = max(e_max, red[w]);
         e_min = min(e_min, red_min[w]);
+        s_min = min(s_min, red_start[w]);
     }
 
-    const int k_begin = split * p.chunk;
-    const int loop_end = min(min(si.kvl, k_begin + p.chunk), e_max);
+    // Tiles wholly before every row's window start are skipped.
+    const int split_begin = split * p.chunk;
+    const int k_begin = max(split_begin, s_min == 0x7fffffff ? 0 : s_min / BN * BN);
+    const int loop_end = min(min(si.kvl, split_begin + p.chunk), e_max);
     const int n_tiles = loop_end > k_begin ? (loop_end - k_begin + BN - 1) / BN : 0;
 
     // Q^T B operands: 8 channels of the row per k-step.
@@ -265,7 +278,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
 #pragma unroll
                     for (int r = 0; r < 16; ++r) {
                         const int key = t0 + kb * 32 + (r >> 2) * 8 + hl * 4 + (r & 3);
-                        if (key >= row_end[qb]) s[kb][qb][r] = sc2 >= 0.f ? -INFINITY : INFINITY;
+                        if (key >= row_end[qb] || key < row_start[qb]) s[kb][qb][r] = sc2 >= 0.f ? -INFINITY : INFINITY;
                     }
             }
             float mx;
@@ -313,7 +326,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
                     float e = __builtin_amdgcn_exp2f(fmaf(s[kb][qb][r], sc2, neg_m));
                     if (MASK) {
                         const int key = t0 + kb * 32 + (r >> 2) * 8 + hl * 4 + (r & 3);
-                        if (key >= row_end[qb]) e = 0.f;
+                        if (key >= row_end[qb] || key < row_start[qb]) e = 0.f;
                     }
                     s[kb][qb][r] = e;
                     lsum += e;
@@ -377,7 +390,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
         qk(kst(S), sc);
         bf16x8 pb[QB][2 * NKB];
         const int t0 = k_begin + i * BN;
-        if (t0 + BN > wmin) {
+        if (t0 + BN > wmin || t0 < wsmax) {
             row_max(t0, sc, std::true_type{});
             probs(t0, sc, pb, std::true_type{});
         } else {
@@ -418,7 +431,8 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
         // it, into the stage that tile t-1 left.
         static_assert(NS >= 4 && NS % 2 == 0 && NKB == 1,
                       "the pipelined schedule uses an even number (>= 4) of LDS stages of 32-key tiles");
-        const int F = sc2 > 0.f ? max(0, min(n_tiles, (e_min - k_begin) / BN)) : 0;
+        // (With a sliding window every tile goes through the masked plain order.)
+        const int F = sc2 > 0.f && a.window == 0 ? max(0, min(n_tiles, (e_min - k_begin) / BN)) : 0;
         const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
         // Segment 1: nxt = raw scores of key block kbn of the K stage; the

@@ -62,7 +62,7 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
     static_assert(NS >= 2 && NS <= 4, "2..4 stages");
 
     __shared__ __attribute__((aligned(16))) uint16_t t0_[TE], t1_[TE], t2_[NS > 2 ? TE : 8], t3_[NS > 3 ? TE : 8];
-    __shared__ int red[NW];
+    __shared__ int red[NW], red_start[NW];
     // Partial-score exchange: [wave][4 chunks][64 lanes] x 16 bytes.
     __shared__ __attribute__((aligned(16))) float xch[NW * 4 * 64 * 4];
     auto stage = [&](int st) -> uint16_t* { return st == 0 ? t0_ : st == 1 ? t1_ : st == 2 ? t2_ : t3_; };
@@ -91,16 +91,29 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
     const int qi = row_ok ? m / H : 0;
     const int head = row_ok ? m - qi * H : 0;
     const int qpos = row_ok ? a.q_pos[si.q0 + qi] : -1;
+    // Visible keys [row_start, row_end): causal, and with a sliding window
+    // also row_start = q_pos - window + 1.
     const int row_end = row_ok ? max(0, min(si.kvl, qpos + 1)) : 0;
+    const int row_start = a.window > 0 && row_ok ? max(0, qpos - a.window + 1) : 0;
     const int wmin = wave_min_i(row_ok ? row_end : 0x7fffffff);
     const int wmax = wave_max_i(row_end);
-    if (lane == 0) red[wave] = wmax;
+    const int wsmin = wave_min_i(row_ok ? row_start : 0x7fffffff);
+    const int wsmax = wave_max_i(row_start);   // tiles below this need the window mask
+    if (lane == 0) {
+        red[wave] = wmax;
+        red_start[wave] = wsmin;
+    }
     __syncthreads();
-    int e_max = 0;
+    int e_max = 0, s_min = 0x7fffffff;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) e_max = max(e_max, red[w]);
-    const int k_begin = split * p.chunk;
-    const int loop_end = min(min(si.kvl, k_begin + p.chunk), e_max);
+    for (int w = 0; w < NW; ++w) {
+        e_max = max(e_max, red[w]);
+        s_min = min(s_min, red_start[w]);
+    }
+    // Tiles wholly before every row's window start are skipped.
+    const int split_begin = split * p.chunk;
+    const int k_begin = max(split_begin, s_min == 0x7fffffff ? 0 : s_min / MBN * MBN);
+    const int loop_end = min(min(si.kvl, split_begin + p.chunk), e_max);
     const int n_tiles = loop_end > k_begin ? (loop_end - k_begin + MBN - 1) / MBN : 0;
 
     bf16x8 qf[KS];
@@ -217,7 +230,7 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int kk = t0 + (r >> 2) * 8 + hl * 4 + (r & 3);
-                if (kk >= row_end) s[r] = sc2 >= 0.f ? -INFINITY : INFINITY;
+                if (kk >= row_end || kk < row_start) s[r] = sc2 >= 0.f ? -INFINITY : INFINITY;
             }
         }
         float mx;
@@ -249,7 +262,7 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
             float e = __builtin_amdgcn_exp2f(fmaf(s[r], sc2, neg_m));
             if (MASK) {
                 const int kk = t0 + (r >> 2) * 8 + hl * 4 + (r & 3);
-                if (kk >= row_end) e = 0.f;
+                if (kk >= row_end || kk < row_start) e = 0.f;
             }
             s[r] = e;
             lsum += e;
@@ -313,7 +326,7 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
                 const int ahead = i + NS - 1;
                 if (ahead < n_tiles) issue(k_begin + ahead * MBN, stage((s + NS - 1) % NS));
                 const int t0 = k_begin + i * MBN;
-                if (t0 + MBN > wmin)
+                if (t0 + MBN > wmin || t0 < wsmax)
                     compute(t0, stage(s), std::true_type{});
                 else
                     compute(t0, stage(s), std::false_type{});

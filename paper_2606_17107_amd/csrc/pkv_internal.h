@@ -77,6 +77,7 @@ struct AttnArgs {
     int32_t max_q;
     int32_t max_kv_len;
     int32_t n_splits;
+    int32_t window;           // 0: full causal; W > 0: slots j > q_pos - W only
     int64_t cache_slots;
     float scale;
     int64_t q_stride[3];

@@ -59,7 +59,7 @@ class pkv_attn_desc(ctypes.Structure):
         ("dtype", ctypes.c_int32), ("variant", ctypes.c_int32), ("n_layers", ctypes.c_int32),
         ("n_seqs", ctypes.c_int32), ("head_dim_v", ctypes.c_int32), ("total_q", ctypes.c_int32),
         ("max_q", ctypes.c_int32), ("max_kv_len", ctypes.c_int32), ("n_splits", ctypes.c_int32),
-        ("reserved", ctypes.c_int32), ("cu_q", ctypes.c_void_p), ("kv_base", ctypes.c_void_p),
+        ("window", ctypes.c_int32), ("cu_q", ctypes.c_void_p), ("kv_base", ctypes.c_void_p),
         ("cache_slots", ctypes.c_int64), ("q_stride", _i64x3), ("k_stride", _i64x3),
         ("v_stride", _i64x3), ("o_stride", _i64x3), ("lse_out", ctypes.c_void_p),
     ]
@@ -236,7 +236,7 @@ def make_attn_desc(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor
                    max_kv_len: int, n_seqs: int = 1, cu_q: Optional[torch.Tensor] = None,
                    kv_base: Optional[torch.Tensor] = None, max_q: Optional[int] = None,
                    variant: int = PKV_ATTN_GQA, n_splits: int = 0,
-                   lse_out: Optional[torch.Tensor] = None) -> pkv_attn_desc:
+                   lse_out: Optional[torch.Tensor] = None, window: int = 0) -> pkv_attn_desc:
     """Descriptor for q [L][rows][H][d], caches [L][Hkv][slots][*], out [L][rows][H][dv]."""
     d = pkv_attn_desc()
     d.dtype = _dtype_code(q)
@@ -248,7 +248,7 @@ def make_attn_desc(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor
     d.max_q = q.shape[1] if max_q is None else int(max_q)
     d.max_kv_len = int(max_kv_len)
     d.n_splits = int(n_splits)
-    d.reserved = 0
+    d.window = int(window)
     d.cu_q = None if cu_q is None else cu_q.data_ptr()
     d.kv_base = None if kv_base is None else kv_base.data_ptr()
     d.cache_slots = k_cache.shape[2]
@@ -271,13 +271,13 @@ def attention_workspace(desc: pkv_attn_desc, n_q_heads: int, n_kv_heads: int, he
 
 def suffix_attention(q, k_cache, v_cache, out, q_pos, kv_len, scale, max_kv_len, n_seqs=1, cu_q=None,
                      kv_base=None, max_q=None, variant=PKV_ATTN_GQA, n_splits=0, lse_out=None,
-                     workspace=None, stream=None) -> None:
+                     workspace=None, stream=None, window=0) -> None:
     """Tensor-level call of pkv_suffix_attention (allocates the workspace with torch if not given)."""
     H = q.shape[2]
     Hkv = k_cache.shape[1]
     D = q.shape[3]
     desc = make_attn_desc(q, k_cache, v_cache, out, max_kv_len, n_seqs, cu_q, kv_base, max_q, variant,
-                          n_splits, lse_out)
+                          n_splits, lse_out, window)
     need = pkv_attention_workspace_size(desc, H, Hkv, D)
     if need and (workspace is None or workspace.numel() * workspace.element_size() < need):
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)

@@ -74,15 +74,22 @@ class Workload:
         row = self.head_dim + (0 if self.mla else self.v_dim)
         return 2 * self.skill_tokens * self.n_layers * self.n_kv_heads * row * self.elem_bytes
 
-    def attn_flops(self) -> int:
-        """Algorithmic flops: 2*(d_qk + d_v) per (query, head, visible key), all layers."""
-        vis = sum(min(self.kv_len, self.ctx_slots + i + 1) for i in range(self.n_q))
+    def attn_flops(self, window: int = 0) -> int:
+        """Algorithmic flops: 2*(d_qk + d_v) per (query, head, visible key), all layers
+        (window > 0: keys j > q_pos - window only)."""
+        vis = 0
+        for i in range(self.n_q):
+            p = self.ctx_slots + i
+            lo = max(0, p - window + 1) if window > 0 else 0
+            vis += max(0, min(self.kv_len, p + 1) - lo)
         return 2 * (self.head_dim + self.v_dim) * self.n_heads * vis * self.n_layers
 
-    def attn_bytes(self) -> int:
-        """Algorithmic bytes: K/V over kv_len read once per layer, Q read, O written."""
+    def attn_bytes(self, window: int = 0) -> int:
+        """Algorithmic bytes: K/V over the slots some query sees read once per layer, Q read,
+        O written."""
         kv_row = self.head_dim if self.mla else self.head_dim + self.v_dim
-        kv = self.kv_len * self.n_kv_heads * kv_row
+        first = max(0, self.ctx_slots - window + 1) if window > 0 else 0
+        kv = (self.kv_len - first) * self.n_kv_heads * kv_row
         qo = self.n_q * self.n_heads * (self.head_dim + self.v_dim)
         return (kv + qo) * self.elem_bytes * self.n_layers
 

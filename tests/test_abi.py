@@ -122,7 +122,7 @@ def test_batched_validation():
 def attn_desc(**kw):
     d = pkv.pkv_attn_desc()
     d.dtype, d.variant, d.n_layers, d.n_seqs, d.head_dim_v = 0, 0, 2, 1, 128
-    d.total_q, d.max_q, d.max_kv_len, d.n_splits, d.reserved = 64, 64, 1000, 0, 0
+    d.total_q, d.max_q, d.max_kv_len, d.n_splits, d.window = 64, 64, 1000, 0, 0
     d.cache_slots = 1000
     d.q_stride = pkv._i64x3(64 * 32 * 128, 32 * 128, 128)
     d.k_stride = pkv._i64x3(8 * 1000 * 128, 1000 * 128, 128)
@@ -146,7 +146,7 @@ def attend(d, H=32, Hkv=8, D=128, q=Q, k=K, v=V, o=O, qp=QP, kl=KL, ws=None, wsb
     ({}, dict(H=30), pkv.PKV_ERR_SHAPE),                      # not a multiple of n_kv_heads
     (dict(n_seqs=2), {}, pkv.PKV_ERR_NULL),                   # cu_q required
     (dict(max_q=10), {}, pkv.PKV_ERR_SHAPE),
-    (dict(reserved=2), {}, pkv.PKV_ERR_SHAPE),
+    (dict(window=-1), {}, pkv.PKV_ERR_SHAPE),
     ({}, dict(D=96), pkv.PKV_ERR_UNSUPPORTED),
     (dict(head_dim_v=64), {}, pkv.PKV_ERR_SHAPE),
     (dict(variant=1), {}, pkv.PKV_ERR_SHAPE),                 # MLA needs 1 KV head, 576/512

@@ -204,3 +204,56 @@ def test_transplant_then_attend_equals_recompute(ref):
     bad_k[:, :, dst] = k_src
     o3, _ = ref.attention(q, bad_k[0], spliced_v[0], q_pos, cap + n_q, 0.125)
     assert np.abs(o3 - o2).max() > 1e-3
+
+
+def sdpa_window_reference(q, k, v, q_pos, kv_len, scale, window):
+    """torch SDPA (fp64) with an explicit banded mask: q_pos - window < j <= q_pos, j < kv_len."""
+    qd = torch.from_numpy(bits_to_f64(q)).permute(1, 0, 2)
+    kd = torch.from_numpy(bits_to_f64(k[:, :kv_len]))
+    vd = torch.from_numpy(bits_to_f64(v[:, :kv_len]))
+    G = qd.shape[0] // kd.shape[0]
+    kd = kd.repeat_interleave(G, dim=0)
+    vd = vd.repeat_interleave(G, dim=0)
+    j = torch.arange(kv_len)[None, :]
+    p = torch.from_numpy(q_pos.astype(np.int64))[:, None]
+    mask = (j <= p) & (j > p - window)
+    o = F.scaled_dot_product_attention(qd, kd, vd, attn_mask=mask, scale=scale)
+    return o.permute(1, 0, 2).numpy()
+
+
+@pytest.mark.parametrize("window", [1, 7, 33, 100, 1000])
+def test_sliding_window_matches_banded_sdpa(ref, window):
+    """Sliding-window layers keep the full cache; the mask alone enforces the window (Sec. 8 config fix)."""
+    H, Hkv, d, n_q, slots = 4, 2, 64, 12, 300
+    q = randn((n_q, H, d), 21, torch.bfloat16, 2.0)
+    k = randn((Hkv, slots, d), 22)
+    v = randn((Hkv, slots, d), 23)
+    q_pos = np.array([0, 5, 31, 32, 64, 99, 150, 200, 250, 280, 290, 299], dtype=np.int32)
+    out, _ = ref.attention(q, k, v, q_pos, slots, 1 / math.sqrt(d), window=window)
+    want = sdpa_window_reference(q, k, v, q_pos, slots, 1 / math.sqrt(d), window)
+    np.testing.assert_allclose(out, want, rtol=1e-12, atol=1e-12)
+
+
+def test_sliding_window_limits(ref):
+    H, Hkv, d, n_q, slots = 4, 1, 32, 6, 80
+    q = randn((n_q, H, d), 24, torch.bfloat16, 3.0)
+    k = randn((Hkv, slots, d), 25)
+    v = randn((Hkv, slots, d), 26)
+    q_pos = np.array([0, 3, 17, 40, 70, 79], dtype=np.int32)
+    full, lse_full = ref.attention(q, k, v, q_pos, slots, 0.2)
+    # a window covering every visible slot is plain causal attention, to the bit
+    wide, lse_wide = ref.attention(q, k, v, q_pos, slots, 0.2, window=80)
+    assert np.array_equal(full, wide) and np.array_equal(lse_full, lse_wide)
+    # window 1: only the query's own slot is visible, so the output is that value row
+    one, lse_one = ref.attention(q, k, v, q_pos, slots, 0.2, window=1)
+    vd = bits_to_f64(v)
+    for i, p in enumerate(q_pos):
+        np.testing.assert_array_equal(one[i], np.broadcast_to(vd[0, p], (H, d)))
+    # windowed attention equals causal attention over the sliced cache with shifted positions
+    for W in (5, 16, 50):
+        win, _ = ref.attention(q, k, v, q_pos, slots, 0.2, window=W)
+        for i, p in enumerate(q_pos):
+            lo = max(0, int(p) - W + 1)
+            sl, _ = ref.attention(np.ascontiguousarray(q[i:i + 1]), np.ascontiguousarray(k[:, lo:]),
+                                  np.ascontiguousarray(v[:, lo:]), np.array([p - lo], np.int32), slots - lo, 0.2)
+            np.testing.assert_allclose(win[i], sl[0], rtol=1e-13, atol=1e-13)
