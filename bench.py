@@ -41,9 +41,20 @@ def log(*a):
 class GqaStep:
     """Inputs and launches of one workload (single sequence, GQA or MLA)."""
 
-    def __init__(self, w: synth.Workload, n_splits: int, seed: int = 0, window: int = 0):
+    def __init__(self, w: synth.Workload, n_splits: int, seed: int = 0, window: int = 0, rope: str = "theta"):
         self.w = w
         self.window = window
+        self.rope = rope
+        # explicit per-pair frequencies for pkv_reposition_splice_freqs (None: the theta schedule)
+        tables = {"mrope_sectioned": lambda: synth.mrope_temporal_omega(w.theta, w.rope_dim, (16, 24, 24)),
+                  "mrope_interleaved": lambda: synth.mrope_temporal_omega(w.theta, w.rope_dim, (24, 20, 20),
+                                                                           "interleaved"),
+                  "llama31": lambda: synth.llama31_omega(w.theta, w.rope_dim)}
+        self.omega = None
+        if rope != "theta":
+            import ctypes
+            t = tables[rope]()
+            self.omega = (ctypes.c_double * len(t))(*[float(x) for x in t])
         dev = torch.device("cuda")
         c = synth.gqa_case(w, seed=seed, device=dev)
         self.cache_k = c["ctx_k"]
@@ -83,8 +94,15 @@ class GqaStep:
 
     def splice(self, stream):
         w = self.w
-        st = pkv.pkv_reposition_splice(self.skill_k, self.skill_v, self.cache_k, self.cache_v, self.src_pos,
-                                       self.dst_pos, w.theta, w.rope_dim, self.splice_layout, stream)
+        if self.omega is not None:
+            import ctypes
+            st = pkv.lib().pkv_reposition_splice_freqs(
+                pkv._ptr(self.skill_k), pkv._ptr(self.skill_v), pkv._ptr(self.cache_k), pkv._ptr(self.cache_v),
+                pkv._ptr(self.src_pos), pkv._ptr(self.dst_pos), None, self.omega, w.rope_dim,
+                ctypes.byref(self.splice_layout), stream)
+        else:
+            st = pkv.pkv_reposition_splice(self.skill_k, self.skill_v, self.cache_k, self.cache_v, self.src_pos,
+                                           self.dst_pos, w.theta, w.rope_dim, self.splice_layout, stream)
         if st != 0:
             raise pkv.PkvError(st, pkv.pkv_last_error())
 
@@ -101,9 +119,10 @@ class GqaStep:
 
     def describe(self):
         w = self.w
-        return ("%s: %d layers, %d/%d heads, d %d, %d-token skill %d->%d, %d-token suffix over %d slots%s"
+        return ("%s: %d layers, %d/%d heads, d %d, %d-token skill %d->%d, %d-token suffix over %d slots%s%s"
                 % (w.name, w.n_layers, w.n_heads, w.n_kv_heads, w.head_dim, w.skill_tokens, w.src_pos0, w.dst_pos0,
-                   w.n_q, w.kv_len, ", sliding window %d" % self.window if self.window else ""))
+                   w.n_q, w.kv_len, ", sliding window %d" % self.window if self.window else "",
+                   ", splice frequencies %s" % self.rope if self.rope != "theta" else ""))
 
     def attn_flops(self):
         return self.w.attn_flops(self.window)
@@ -384,6 +403,9 @@ def main():
                     help="keep warming up until this much wall time has passed (clock ramp)")
     ap.add_argument("--workload", default="gqa8b", choices=sorted(synth.WORKLOADS) + ["batched"])
     ap.add_argument("--splits", type=int, default=0, help="KV splits for attention (0 = library choice)")
+    ap.add_argument("--rope", default="theta", choices=["theta", "mrope_sectioned", "mrope_interleaved", "llama31"],
+                    help="splice frequencies: the theta schedule, or an explicit table through "
+                         "pkv_reposition_splice_freqs (M-RoPE temporal move, Llama-3.1 scaling)")
     ap.add_argument("--window", type=int, default=0,
                     help="sliding-window attention over the full cache (0 = causal; single-sequence workloads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -408,7 +430,7 @@ def main():
         step = BatchedStep(w, args.splits)
     else:
         w = synth.WORKLOADS[args.workload]
-        step = GqaStep(w, args.splits, window=args.window)
+        step = GqaStep(w, args.splits, window=args.window, rope=args.rope)
     log("workload", w)
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream

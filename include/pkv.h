@@ -125,6 +125,31 @@ pkv_status pkv_reposition_splice(const void* src_k, const void* src_v, void* dst
                                  const int32_t* src_pos, const int32_t* dst_pos, float rope_theta,
                                  int32_t rope_dim, const pkv_layout* layout, void* stream);
 
+/* Reposition + splice with explicit per-pair frequencies: as
+ * pkv_reposition_splice, with pair i of the rotary slice turned by
+ * delta_t * omega[i] instead of delta_t * rope_theta^(-2i/rope_dim).  This
+ * covers the RoPE extensions the method also applies to (Related work: rotary
+ * embeddings and their extensions): rescaled frequency schedules (Llama-3.1
+ * style, YaRN; the rotation stays a pure rotation), and M-RoPE (Sec. 8
+ * "Multimodal"; Fig. "attention-variant adapters" (b)), where each rotary
+ * pair belongs to the temporal, height or width axis: moving an image along
+ * the trajectory by delta temporal positions passes omega[i] for the temporal
+ * pairs and 0 for the spatial ones, whose channels then come through
+ * bit-exact (cos 0 = 1, sin 0 = 0).  src_pos / dst_pos are the positions on
+ * the axis being moved (delta_t = dst_pos[t] - src_pos[t]).
+ * dst_slot: optional device int32 [n_tokens], the destination cache slot of
+ * each token; NULL means slot = dst_pos[t] as in pkv_reposition_splice.  With
+ * M-RoPE the tokens of an image share one temporal position, so the slots are
+ * given separately.  Out-of-range slots are skipped and flagged as there.
+ * omega: host fp64 [rope_dim/2], read during the call only (any finite
+ * values).  rope_dim <= 256.
+ * Errors: as pkv_reposition_splice; PKV_ERR_NULL for a NULL omega,
+ * PKV_ERR_SHAPE for a non-finite entry. */
+pkv_status pkv_reposition_splice_freqs(const void* src_k, const void* src_v, void* dst_k, void* dst_v,
+                                       const int32_t* src_pos, const int32_t* dst_pos, const int32_t* dst_slot,
+                                       const double* omega, int32_t rope_dim, const pkv_layout* layout,
+                                       void* stream);
+
 /* One chunk of a multi-chunk composition (Sec. 5: a library of skills
  * composes; Sec. 7 E4: memory split into independently precompiled blocks).
  * Source tokens src_slot0 .. src_slot0+n_tokens-1 were encoded at positions

@@ -57,11 +57,11 @@ def _load():
     lib.pkvref_rope_omega.argtypes = [f64, ctypes.c_int, ctypes.c_int]
     lib.pkvref_rope_rows.restype = None
     lib.pkvref_rope_rows.argtypes = [ctypes.c_int, P, P, i64, ctypes.c_int, P, f64, ctypes.c_int,
-                                     ctypes.c_int, ctypes.c_int]
+                                     ctypes.c_int, ctypes.c_int, P]
     lib.pkvref_reposition_splice.restype = i64
     lib.pkvref_reposition_splice.argtypes = [
         ctypes.c_int, P, P, P, P, P, P, i64, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-        f64, ctypes.c_int, ctypes.c_int, ctypes.c_int, P, P, P, P, i64]
+        f64, ctypes.c_int, ctypes.c_int, ctypes.c_int, P, P, P, P, i64, P, P]
     lib.pkvref_attention.restype = None
     lib.pkvref_attention.argtypes = [
         ctypes.c_int, P, P, P, P, P, P, i64, i64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -106,24 +106,34 @@ def rope_omega(theta: float, r: int, i: int) -> float:
     return float(_load().pkvref_rope_omega(float(theta), int(r), int(i)))
 
 
+def _omega_arg(omega, rope_dim):
+    if omega is None:
+        return None, None
+    w = np.ascontiguousarray(omega, dtype=np.float64)
+    assert w.shape == (rope_dim // 2,), "omega needs one frequency per rotary pair"
+    return w, _ptr(w)
+
+
 def rope_rows(x: np.ndarray, pos: np.ndarray, theta: float, rope_dim: int, rope_offset: int = 0,
-              style: int = HALF) -> np.ndarray:
+              style: int = HALF, omega=None) -> np.ndarray:
     """Return R(pos[row]) x[row] for every row of ``x`` (last axis = channels).
 
-    ``pos`` has one int32 position per row (shape ``x.shape[:-1]``)."""
+    ``pos`` has one int32 position per row (shape ``x.shape[:-1]``).  ``omega``:
+    optional per-pair frequencies replacing theta^(-2i/rope_dim)."""
     x = np.ascontiguousarray(x)
     d = x.shape[-1]
     n_rows = x.size // d
     pos = np.ascontiguousarray(np.broadcast_to(pos, x.shape[:-1]), dtype=np.int32).reshape(-1)
     assert pos.size == n_rows
     out = np.empty_like(x)
+    w, wp = _omega_arg(omega, rope_dim)
     _load().pkvref_rope_rows(_dtype_code(x), _ptr(x), _ptr(out), n_rows, d, _ptr(pos), float(theta),
-                             int(rope_dim), int(rope_offset), int(style))
+                             int(rope_dim), int(rope_offset), int(style), wp)
     return out
 
 
 def reposition_splice(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, theta, rope_dim, rope_offset=0,
-                      style=HALF, dst_capacity=None) -> int:
+                      style=HALF, dst_capacity=None, omega=None, dst_slot=None) -> int:
     """Splice ``src_k``/``src_v`` ``[L][Hkv][T][*]`` into ``dst_k``/``dst_v`` in place.
 
     dst_k[l][h][dst_pos[t]] = R(dst_pos[t] - src_pos[t]) src_k[l][h][t]; V copied.
@@ -136,6 +146,8 @@ def reposition_splice(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, theta, rope_
     src_pos = np.ascontiguousarray(src_pos, dtype=np.int32)
     dst_pos = np.ascontiguousarray(dst_pos, dtype=np.int32)
     assert src_pos.size == T and dst_pos.size == T
+    slots = None if dst_slot is None else np.ascontiguousarray(dst_slot, dtype=np.int32)
+    assert slots is None or slots.size == T
     cap = dst_k.shape[2] if dst_capacity is None else int(dst_capacity)
     sks = np.array(_estrides(src_k)[:3], dtype=np.int64)
     dks = np.array(_estrides(dst_k)[:3], dtype=np.int64)
@@ -147,7 +159,7 @@ def reposition_splice(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, theta, rope_
     return int(_load().pkvref_reposition_splice(
         dt, _ptr(src_k), _ptr(src_v), _ptr(dst_k), _ptr(dst_v), _ptr(src_pos), _ptr(dst_pos), T, L, H,
         d, v_dim, float(theta), int(rope_dim), int(rope_offset), int(style), _ptr(sks), _ptr(svs),
-        _ptr(dks), _ptr(dvs), cap))
+        _ptr(dks), _ptr(dvs), cap, _omega_arg(omega, rope_dim)[1], _ptr(slots)))
 
 
 def attention(q, k, v, q_pos, kv_len, scale, window=0):

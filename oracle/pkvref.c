@@ -16,6 +16,13 @@
  *         (a cos(p omega_i) - b sin(p omega_i),  a sin(p omega_i) + b cos(p omega_i)).
  *     HALF pairing: (a, b) = (x[o+i], x[o+i+r/2]); INTERLEAVED: (x[o+2i], x[o+2i+1]).
  *     Channels outside [o, o+r) are untouched.
+ *     An explicit per-pair table omega[i] may replace the theta schedule: the
+ *     paper's repositioning also covers the RoPE extensions (Related work:
+ *     rotary embeddings and their extensions), i.e. rescaled frequencies, and
+ *     M-RoPE, whose rotary pairs belong to temporal / height / width axes
+ *     (Sec. 8 "Multimodal"; Fig. "attention-variant adapters" (b)): moving an
+ *     image along the trajectory re-rotates only the temporal pairs, which is
+ *     the table with omega[i] = 0 on the spatial pairs.
  *   - Reposition + splice (Sec. 5, "From mechanism to prediction"; Fig. "Two
  *     cache operations" (b); App. B skill example): the cached keys are
  *     post-RoPE, so a chunk cached at source positions is moved to target
@@ -114,13 +121,13 @@ static void ref_pair_index(int style, int o, int r, int i, int* ia, int* ib) {
  * out = R(p) in, channels outside the rotary slice copied bit-exact.
  * in and out may be different arrays; in_off/out_off are element offsets. */
 static void ref_rotate_row(int dtype, const void* in, int64_t in_off, void* out, int64_t out_off,
-                           int d, double p, double theta, int r, int o, int style) {
+                           int d, double p, double theta, int r, int o, int style, const double* omega) {
     for (int c = 0; c < d; ++c)
         if (c < o || c >= o + r) ref_copy_elem(out, in, dtype, out_off + c, in_off + c);
     for (int i = 0; i < r / 2; ++i) {
         int ia, ib;
         ref_pair_index(style, o, r, i, &ia, &ib);
-        double ang = p * pkvref_rope_omega(theta, r, i);
+        double ang = p * (omega ? omega[i] : pkvref_rope_omega(theta, r, i));
         double cs = cos(ang), sn = sin(ang);
         double a = ref_load(in, dtype, in_off + ia);
         double b = ref_load(in, dtype, in_off + ib);
@@ -131,13 +138,15 @@ static void ref_rotate_row(int dtype, const void* in, int64_t in_off, void* out,
 
 /* RoPE at per-row positions: out[row] = R(pos[row]) in[row] for rows laid out
  * contiguously with n_rows x d elements.  Used to build post-RoPE keys and
- * queries from pre-RoPE draws. */
+ * queries from pre-RoPE draws.  omega: NULL (theta schedule) or rope_dim/2
+ * per-pair frequencies. */
 void pkvref_rope_rows(int dtype, const void* in, void* out, int64_t n_rows, int d,
-                      const int32_t* pos, double theta, int rope_dim, int rope_offset, int style) {
+                      const int32_t* pos, double theta, int rope_dim, int rope_offset, int style,
+                      const double* omega) {
 #pragma omp parallel for schedule(static)
     for (int64_t row = 0; row < n_rows; ++row)
         ref_rotate_row(dtype, in, row * d, out, row * d, d, (double)pos[row], theta, rope_dim,
-                       rope_offset, style);
+                       rope_offset, style, omega);
 }
 
 /* Reposition + splice.  For every layer l, KV head h and skill token t:
@@ -146,28 +155,34 @@ void pkvref_rope_rows(int dtype, const void* in, void* out, int64_t n_rows, int 
  * Strides are in elements: {layer, head, token}; channels are contiguous.
  * v_dim == 0 means no V tensor (MLA: the latent lives in the K row and is the
  * non-rotary part of it).  A token whose dst_pos falls outside
- * [0, dst_capacity) is skipped; the return value counts skipped tokens. */
+ * [0, dst_capacity) is skipped; the return value counts skipped tokens.
+ * omega: NULL (theta schedule) or rope_dim/2 per-pair frequencies.
+ * dst_slot: NULL (the destination slot is dst_pos[t]) or the slot of each
+ * token, for layouts where positions and cache slots differ (M-RoPE images,
+ * whose tokens share one temporal position). */
 int64_t pkvref_reposition_splice(int dtype, const void* src_k, const void* src_v, void* dst_k,
                                  void* dst_v, const int32_t* src_pos, const int32_t* dst_pos,
                                  int64_t n_tokens, int n_layers, int n_kv_heads, int head_dim,
                                  int v_dim, double theta, int rope_dim, int rope_offset, int style,
                                  const int64_t* src_k_stride, const int64_t* src_v_stride,
                                  const int64_t* dst_k_stride, const int64_t* dst_v_stride,
-                                 int64_t dst_capacity) {
+                                 int64_t dst_capacity, const double* omega, const int32_t* dst_slot) {
     int64_t skipped = 0;
-    for (int64_t t = 0; t < n_tokens; ++t)
-        if (dst_pos[t] < 0 || dst_pos[t] >= dst_capacity) ++skipped;
+    for (int64_t t = 0; t < n_tokens; ++t) {
+        int64_t slot = dst_slot ? dst_slot[t] : dst_pos[t];
+        if (slot < 0 || slot >= dst_capacity) ++skipped;
+    }
 #pragma omp parallel for collapse(2) schedule(static)
     for (int l = 0; l < n_layers; ++l) {
         for (int h = 0; h < n_kv_heads; ++h) {
             for (int64_t t = 0; t < n_tokens; ++t) {
-                int64_t slot = dst_pos[t];
+                int64_t slot = dst_slot ? dst_slot[t] : dst_pos[t];
                 if (slot < 0 || slot >= dst_capacity) continue;
                 double delta = (double)dst_pos[t] - (double)src_pos[t];
                 int64_t sk = l * src_k_stride[0] + h * src_k_stride[1] + t * src_k_stride[2];
                 int64_t dk = l * dst_k_stride[0] + h * dst_k_stride[1] + slot * dst_k_stride[2];
                 ref_rotate_row(dtype, src_k, sk, dst_k, dk, head_dim, delta, theta, rope_dim,
-                               rope_offset, style);
+                               rope_offset, style, omega);
                 if (v_dim > 0) {
                     int64_t sv = l * src_v_stride[0] + h * src_v_stride[1] + t * src_v_stride[2];
                     int64_t dv = l * dst_v_stride[0] + h * dst_v_stride[1] + slot * dst_v_stride[2];

@@ -256,6 +256,25 @@ PKV_EXPORT pkv_status pkv_reposition_splice(const void* src_k, const void* src_v
     return device_status(pkv::launch_splice(a, (hipStream_t)stream), "reposition_splice launch");
 }
 
+PKV_EXPORT pkv_status pkv_reposition_splice_freqs(const void* src_k, const void* src_v, void* dst_k,
+                                                  void* dst_v, const int32_t* src_pos, const int32_t* dst_pos,
+                                                  const int32_t* dst_slot, const double* omega, int32_t rope_dim,
+                                                  const pkv_layout* layout, void* stream) {
+    pkv::SpliceArgs a;
+    pkv_status st = check_splice(src_k, src_v, dst_k, dst_v, 1.0f, rope_dim, layout, true, a);
+    if (st != PKV_OK) return st;
+    if (!src_pos || !dst_pos) return fail(PKV_ERR_NULL, "src_pos and dst_pos are required");
+    if (!omega) return fail(PKV_ERR_NULL, "omega is required");
+    for (int i = 0; i < rope_dim / 2; ++i)
+        if (!isfinite(omega[i])) return fail(PKV_ERR_SHAPE, "omega[%d] is not finite", i);
+    a.src_pos = src_pos;
+    a.dst_pos = dst_pos;
+    a.dst_slot = dst_slot;
+    a.omega = omega;
+    if (a.n_tokens == 0) return ok();
+    return device_status(pkv::launch_splice(a, (hipStream_t)stream), "reposition_splice_freqs launch");
+}
+
 PKV_EXPORT pkv_status pkv_reposition_splice_batched(const void* src_k, const void* src_v, void* dst_k,
                                                     void* dst_v, const pkv_segment* segs, int32_t n_segs,
                                                     int32_t max_seg_tokens, float rope_theta,

@@ -26,6 +26,7 @@ struct SpliceArgs {
     // per-token mode
     const int32_t* src_pos;
     const int32_t* dst_pos;
+    const int32_t* dst_slot;  // destination slots, or null (slot = dst_pos)
     // segment mode
     const SpliceSegment* segs;
     int32_t n_segs;
@@ -42,6 +43,7 @@ struct SpliceArgs {
     int64_t n_tokens;        // per-token mode: tokens; segment mode: source slots
     int64_t dst_capacity;
     double theta;
+    const double* omega;      // host, rope_dim/2 per-pair frequencies, or null (theta schedule)
     int64_t src_k_stride[3];  // elements
     int64_t src_v_stride[3];
     int64_t dst_k_stride[3];

@@ -136,6 +136,15 @@ __device__ inline void delta_sincos(int64_t delta, double omega, float& c, float
     c = ((q + 1) & 2) ? -ca : ca;
 }
 
+// Explicit per-pair frequencies (scaled RoPE, or M-RoPE with the spatial pairs
+// at zero); an empty argument when the theta schedule is used.
+template <bool TAB>
+struct FreqArg {};
+template <>
+struct FreqArg<true> {
+    double w[1 << kPairBits];
+};
+
 __device__ inline double pair_omega(int pair, const Geo& g) {
     double w = 1.0;
 #pragma unroll
@@ -208,9 +217,17 @@ __device__ inline int lane_pair(int l, int j, int half_r) {
         return j < CE / 2 ? l * (CE / 2) + j : (half_r + l) * (CE / 2) + (j - CE / 2);
 }
 
-template <int EB, int STYLE, bool SEG>
-__global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g) {
+template <int EB, int STYLE, bool SEG, bool TAB>
+__global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, FreqArg<TAB> ft) {
     constexpr int CE = 16 / EB;   // elements per 16-byte chunk = pairs per rotary lane
+    // Explicit frequencies: lane l holds those of pairs l and 64 + l, loaded
+    // before anything else so that waiting for them leaves the later loads in
+    // flight; other lanes' pairs are gathered by shuffle.
+    double w_lo = 0.0, w_hi = 0.0;
+    if constexpr (TAB) {
+        w_lo = ft.w[__lane_id()];
+        w_hi = ft.w[kWave + __lane_id()];
+    }
     const int grp = blockIdx.y;
     const uint32_t tid = threadIdx.x;
     const uint32_t tl = g.lanes == 1 ? tid : __umulhi(tid, g.lanes_magic);   // tid / lanes, exact here
@@ -296,7 +313,7 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g) {
         int64_t src_slot, dst_slot = -1, delta = 0;
         const bool present = in_tile && t < n_tok;   // a token of the chunk (or segment)
         bool active;                                 // ... whose source row can be read
-        int32_t dp = 0, spos = 0;
+        int32_t dp = 0, spos = 0, dslot = 0;
         if constexpr (SEG) {
             src_slot = sg.src_slot0 + t;
             active = present && src_slot >= 0 && src_slot < a.n_tokens;
@@ -309,6 +326,7 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g) {
             src_slot = active ? t : a.n_tokens - 1;
             dp = a.dst_pos[src_slot];
             spos = a.src_pos[src_slot];
+            if (a.dst_slot) dslot = a.dst_slot[src_slot];
         }
         const char* sbase = src_t + src_slot * s2 * EB;
 
@@ -333,7 +351,7 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g) {
         load_rows(r0);
 
         if constexpr (!SEG) {
-            dst_slot = dp;
+            dst_slot = a.dst_slot ? dslot : dp;   // slots follow positions unless given
             delta = (int64_t)dp - (int64_t)spos;
         }
         const bool valid = dst_slot >= 0 && dst_slot < a.dst_capacity;
@@ -352,13 +370,26 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g) {
                 if (d_ref != 0) {
                     float c1 = 1.0f, s1v = 0.0f;
                     const int j = __lane_id();
-                    if (j < g.n_pairs) delta_sincos(d_ref, pair_omega(j, g), c1, s1v);
+                    if (j < g.n_pairs) delta_sincos(d_ref, TAB ? w_lo : pair_omega(j, g), c1, s1v);
 #pragma unroll
                     for (int e = 0; e < CE; ++e) {
                         const int src = rope ? lane_pair<CE, STYLE>(lane, e, half_r) : 0;
                         cs[e] = __shfl(c1, src);
                         sn[e] = __shfl(s1v, src);
                     }
+                }
+            } else if constexpr (TAB) {
+                // every lane takes part in the shuffles (the branch is wave-uniform)
+                double wp[CE];
+#pragma unroll
+                for (int e = 0; e < CE; ++e) {
+                    const int pr = rope ? lane_pair<CE, STYLE>(lane, e, half_r) : 0;
+                    const double lo = __shfl(w_lo, pr & (kWave - 1)), hi = __shfl(w_hi, pr & (kWave - 1));
+                    wp[e] = pr < kWave ? lo : hi;
+                }
+                if (rope && delta != 0) {
+#pragma unroll
+                    for (int e = 0; e < CE; ++e) delta_sincos(delta, wp[e], cs[e], sn[e]);
                 }
             } else if (rope && delta != 0) {
 #pragma unroll
@@ -392,10 +423,20 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g) {
 
 template <int EB, int STYLE>
 hipError_t launch_typed(const SpliceArgs& a, const Geo& g, dim3 grid, dim3 block, hipStream_t st) {
-    if (a.segs)
-        hipLaunchKernelGGL((splice_kernel<EB, STYLE, true>), grid, block, 0, st, a, g);
-    else
-        hipLaunchKernelGGL((splice_kernel<EB, STYLE, false>), grid, block, 0, st, a, g);
+    if (a.omega) {
+        FreqArg<true> ft;
+        for (int i = 0; i < (1 << kPairBits); ++i) ft.w[i] = i < g.n_pairs ? a.omega[i] : 0.0;
+        if (a.segs)
+            hipLaunchKernelGGL((splice_kernel<EB, STYLE, true, true>), grid, block, 0, st, a, g, ft);
+        else
+            hipLaunchKernelGGL((splice_kernel<EB, STYLE, false, true>), grid, block, 0, st, a, g, ft);
+    } else {
+        const FreqArg<false> ft;
+        if (a.segs)
+            hipLaunchKernelGGL((splice_kernel<EB, STYLE, true, false>), grid, block, 0, st, a, g, ft);
+        else
+            hipLaunchKernelGGL((splice_kernel<EB, STYLE, false, false>), grid, block, 0, st, a, g, ft);
+    }
     return hipGetLastError();
 }
 

@@ -65,8 +65,8 @@ class pkv_attn_desc(ctypes.Structure):
     ]
 
 
-SYMBOLS = ("pkv_reposition_splice", "pkv_reposition_splice_batched", "pkv_attention_workspace_size",
-           "pkv_suffix_attention", "pkv_last_error", "pkv_version")
+SYMBOLS = ("pkv_reposition_splice", "pkv_reposition_splice_freqs", "pkv_reposition_splice_batched",
+           "pkv_attention_workspace_size", "pkv_suffix_attention", "pkv_last_error", "pkv_version")
 
 _lib = None
 
@@ -90,6 +90,9 @@ def lib() -> ctypes.CDLL:
     L.pkv_reposition_splice.restype = ctypes.c_int
     L.pkv_reposition_splice.argtypes = [P, P, P, P, P, P, ctypes.c_float, ctypes.c_int32,
                                         ctypes.POINTER(pkv_layout), P]
+    L.pkv_reposition_splice_freqs.restype = ctypes.c_int
+    L.pkv_reposition_splice_freqs.argtypes = [P, P, P, P, P, P, P, ctypes.POINTER(ctypes.c_double),
+                                              ctypes.c_int32, ctypes.POINTER(pkv_layout), P]
     L.pkv_reposition_splice_batched.restype = ctypes.c_int
     L.pkv_reposition_splice_batched.argtypes = [P, P, P, P, P, ctypes.c_int32, ctypes.c_int32,
                                                 ctypes.c_float, ctypes.c_int32, ctypes.POINTER(pkv_layout), P]
@@ -135,6 +138,16 @@ def pkv_reposition_splice(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, rope_the
     return lib().pkv_reposition_splice(_ptr(src_k), _ptr(src_v), _ptr(dst_k), _ptr(dst_v), _ptr(src_pos),
                                        _ptr(dst_pos), float(rope_theta), int(rope_dim),
                                        ctypes.byref(layout) if layout is not None else None, _stream(stream))
+
+
+def pkv_reposition_splice_freqs(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, dst_slot, omega, rope_dim, layout,
+                                stream=None) -> int:
+    w = None
+    if omega is not None:
+        w = (ctypes.c_double * len(omega))(*[float(x) for x in omega])
+    return lib().pkv_reposition_splice_freqs(_ptr(src_k), _ptr(src_v), _ptr(dst_k), _ptr(dst_v), _ptr(src_pos),
+                                             _ptr(dst_pos), _ptr(dst_slot), w, int(rope_dim),
+                                             ctypes.byref(layout) if layout is not None else None, _stream(stream))
 
 
 def pkv_reposition_splice_batched(src_k, src_v, dst_k, dst_v, segs, n_segs, max_seg_tokens, rope_theta,
@@ -211,6 +224,15 @@ def reposition_splice(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, rope_theta, 
     layout = make_layout(src_k, src_v, dst_k, dst_v, rope_offset, rope_style, err_flag=err_flag)
     _check(pkv_reposition_splice(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, rope_theta, rope_dim, layout,
                                  stream))
+
+
+def reposition_splice_freqs(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, omega, rope_dim, rope_offset=0,
+                            rope_style=PKV_ROPE_HALF, dst_slot=None, err_flag=None, stream=None) -> None:
+    """Tensor-level call of pkv_reposition_splice_freqs (per-pair frequencies ``omega``; optional
+    destination slots, else slot = dst_pos)."""
+    layout = make_layout(src_k, src_v, dst_k, dst_v, rope_offset, rope_style, err_flag=err_flag)
+    _check(pkv_reposition_splice_freqs(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, dst_slot, omega, rope_dim,
+                                       layout, stream))
 
 
 def make_segments(segs: Sequence[dict], device) -> torch.Tensor:

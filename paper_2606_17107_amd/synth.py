@@ -252,6 +252,59 @@ def batched_case(bw: BatchedWorkload, plan, seed: int = 0, device="cpu", layers:
     return out
 
 
+# ---- rotary frequency tables (model configuration inputs of the splice) ----
+
+def rope_omega(theta: float, rope_dim: int) -> np.ndarray:
+    """The plain RoPE schedule theta^(-2i/r), i < r/2."""
+    return theta ** (-2.0 * np.arange(rope_dim // 2, dtype=np.float64) / rope_dim)
+
+
+def mrope_axes(rope_dim: int, sections=(16, 24, 24), layout: str = "sectioned") -> np.ndarray:
+    """Axis (0 temporal, 1 height, 2 width) of each rotary pair of an M-RoPE head.
+
+    sectioned: the first sections[0] pairs are temporal, the next sections[1]
+    height, the rest width (the Qwen2.5-VL layout).  interleaved: pairs cycle
+    temporal, height, width while each axis has pairs left in its section, and
+    the remainder goes to the first axis that still has some (the Qwen3-VL
+    layout spreads every axis over the whole frequency range)."""
+    n = rope_dim // 2
+    assert sum(sections) == n
+    axes = np.empty(n, dtype=np.int32)
+    if layout == "sectioned":
+        axes[:] = np.repeat(np.arange(3), sections)
+        return axes
+    assert layout == "interleaved"
+    left = list(sections)
+    for i in range(n):
+        a = i % 3
+        if left[a] == 0:
+            a = next(k for k in range(3) if left[k] > 0)
+        axes[i] = a
+        left[a] -= 1
+    return axes
+
+
+def mrope_temporal_omega(theta: float, rope_dim: int, sections=(16, 24, 24), layout: str = "sectioned"):
+    """Frequencies that move an M-RoPE key along the temporal axis only: the plain
+    schedule on the temporal pairs, zero on the height and width pairs."""
+    return np.where(mrope_axes(rope_dim, sections, layout) == 0, rope_omega(theta, rope_dim), 0.0)
+
+
+def llama31_omega(theta: float, rope_dim: int, factor: float = 8.0, low_freq_factor: float = 1.0,
+                  high_freq_factor: float = 4.0, original_max_position: int = 8192) -> np.ndarray:
+    """The Llama-3.1 rescaled schedule: wavelengths shorter than
+    original/high_freq_factor keep their frequency, longer than
+    original/low_freq_factor are divided by `factor`, and the band between is
+    interpolated linearly in original/wavelength."""
+    w = rope_omega(theta, rope_dim)
+    wavelen = 2.0 * math.pi / w
+    low_wl = original_max_position / low_freq_factor
+    high_wl = original_max_position / high_freq_factor
+    smooth = (original_max_position / wavelen - low_freq_factor) / (high_freq_factor - low_freq_factor)
+    mid = (1.0 - smooth) * w / factor + smooth * w
+    return np.where(wavelen < high_wl, w, np.where(wavelen > low_wl, w / factor, mid))
+
+
 def batched_segments(plan):
     """Segment records (pkv_segment fields) of the batched composition: one per
     (sequence, skill), in sequence order."""

@@ -175,3 +175,17 @@ def test_workspace_size_and_requirement():
     assert pkv.pkv_attention_workspace_size(attn_desc(dtype=1), 32, 8, 128) == 0
     assert pkv.pkv_attention_workspace_size(None, 32, 8, 128) == 0
     assert pkv.pkv_attention_workspace_size(d, 30, 8, 128) == 0
+
+
+def test_freqs_validation():
+    L = good_layout()
+    f = pkv.pkv_reposition_splice_freqs
+    w = [0.5] * 64
+    assert f(SK, SV, DK, DV, SP, DP, None, None, 128, L, 0) == pkv.PKV_ERR_NULL        # omega required
+    assert f(SK, SV, DK, DV, None, DP, None, w, 128, L, 0) == pkv.PKV_ERR_NULL
+    bad = list(w)
+    bad[7] = float("nan")
+    assert f(SK, SV, DK, DV, SP, DP, None, bad, 128, L, 0) == pkv.PKV_ERR_SHAPE
+    assert "omega[7]" in pkv.pkv_last_error()
+    assert f(SK, SV, DK, DV, SP, DP, None, w, 127, L, 0) == pkv.PKV_ERR_SHAPE          # odd rope_dim
+    assert f(SK, SV, DK + 4096 - 4096 + 8, DV, SP, DP, None, w, 128, L, 0) == pkv.PKV_ERR_ALIGN
