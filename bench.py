@@ -41,10 +41,14 @@ def log(*a):
 class GqaStep:
     """Inputs and launches of one workload (single sequence, GQA or MLA)."""
 
-    def __init__(self, w: synth.Workload, n_splits: int, seed: int = 0, window: int = 0, rope: str = "theta"):
+    def __init__(self, w: synth.Workload, n_splits: int, seed: int = 0, window: int = 0, rope: str = "theta",
+                 page_size: int = 0):
         self.w = w
         self.window = window
         self.rope = rope
+        self.page_size = page_size
+        if page_size and rope != "theta":
+            raise SystemExit("--paged takes the theta schedule (no --rope table)")
         # explicit per-pair frequencies for pkv_reposition_splice_freqs (None: the theta schedule)
         tables = {"mrope_sectioned": lambda: synth.mrope_temporal_omega(w.theta, w.rope_dim, (16, 24, 24)),
                   "mrope_interleaved": lambda: synth.mrope_temporal_omega(w.theta, w.rope_dim, (24, 20, 20),
@@ -88,12 +92,53 @@ class GqaStep:
         variant = pkv.PKV_ATTN_MLA if w.mla else pkv.PKV_ATTN_GQA
         self.desc = pkv.make_attn_desc(self.q, self.cache_k, self.v_view, self.out, w.kv_len, variant=variant,
                                        n_splits=n_splits, window=window)
+        if page_size:
+            self._to_pages(page_size, seed)
         self.ws_bytes = pkv.pkv_attention_workspace_size(self.desc, w.n_heads, w.n_kv_heads, w.head_dim)
         self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device=dev)
         torch.cuda.synchronize()
 
+    def _to_pages(self, B: int, seed: int):
+        """Move the cache into a pool [layer][page][slot][kv_head][d] (the vLLM layout) whose pages the
+        block table hands out in a random order, and describe both calls over the pool."""
+        w = self.w
+        dev = self.cache_k.device
+        max_pages = (w.kv_len + B - 1) // B
+        n_pages = max_pages + 64
+        perm = torch.randperm(n_pages, generator=torch.Generator().manual_seed(seed + 101))[:max_pages]
+        self.block_table = perm.to(torch.int32).reshape(1, max_pages).to(dev)
+        p = torch.arange(w.kv_len, device=dev)
+        page, slot = self.block_table[0, p // B].long(), p % B
+        self.pool_k = torch.zeros(w.n_layers, n_pages, B, w.n_kv_heads, w.head_dim, dtype=self.cache_k.dtype,
+                                  device=dev)
+        self.pool_k[:, page, slot] = self.cache_k.permute(0, 2, 1, 3)
+        self.pool_v = None
+        if self.cache_v is not None:
+            self.pool_v = torch.zeros(w.n_layers, n_pages, B, w.n_kv_heads, w.v_dim, dtype=self.cache_v.dtype,
+                                      device=dev)
+            self.pool_v[:, page, slot] = self.cache_v.permute(0, 2, 1, 3)
+        self.cache_k = self.cache_v = self.v_view = None
+        self.pool_v_view = self.pool_k[..., : w.v_dim] if w.mla else self.pool_v
+        self.paging = pkv.make_paging(self.block_table, self.pool_k, self.pool_v_view)
+        L = self.splice_layout
+        L.dst_capacity = max_pages * B
+        L.dst_k_stride = pkv.pool_strides3(self.pool_k)
+        L.dst_v_stride = pkv.pool_strides3(self.pool_v)
+        d = self.desc
+        d.cache_slots = max_pages * B
+        d.k_stride = pkv.pool_strides3(self.pool_k)
+        d.v_stride = pkv.pool_strides3(self.pool_v_view)
+        torch.cuda.synchronize()
+
     def splice(self, stream):
         w = self.w
+        if self.page_size:
+            st = pkv.pkv_reposition_splice_paged(self.skill_k, self.skill_v, self.pool_k, self.pool_v, self.src_pos,
+                                                 self.dst_pos, w.theta, w.rope_dim, self.splice_layout, self.paging,
+                                                 stream)
+            if st != 0:
+                raise pkv.PkvError(st, pkv.pkv_last_error())
+            return
         if self.omega is not None:
             import ctypes
             st = pkv.lib().pkv_reposition_splice_freqs(
@@ -108,6 +153,13 @@ class GqaStep:
 
     def attention(self, stream):
         w = self.w
+        if self.page_size:
+            st = pkv.pkv_suffix_attention_paged(self.q, self.pool_k, self.pool_v_view, self.out, self.q_pos,
+                                                self.kv_len, w.n_heads, w.n_kv_heads, w.head_dim, w.scale, self.desc,
+                                                self.paging, self.ws, self.ws_bytes, stream)
+            if st != 0:
+                raise pkv.PkvError(st, pkv.pkv_last_error())
+            return
         st = pkv.pkv_suffix_attention(self.q, self.cache_k, self.v_view, self.out, self.q_pos, self.kv_len,
                                       w.n_heads, w.n_kv_heads, w.head_dim, w.scale, self.desc, self.ws,
                                       self.ws_bytes, stream)
@@ -122,7 +174,9 @@ class GqaStep:
         return ("%s: %d layers, %d/%d heads, d %d, %d-token skill %d->%d, %d-token suffix over %d slots%s%s"
                 % (w.name, w.n_layers, w.n_heads, w.n_kv_heads, w.head_dim, w.skill_tokens, w.src_pos0, w.dst_pos0,
                    w.n_q, w.kv_len, ", sliding window %d" % self.window if self.window else "",
-                   ", splice frequencies %s" % self.rope if self.rope != "theta" else ""))
+                   ", splice frequencies %s" % self.rope if self.rope != "theta" else "")
+                + (", paged cache (%d-slot pages, shuffled block table, [layer][page][slot][kv_head][d] pool)"
+                   % self.page_size if self.page_size else ""))
 
     def attn_flops(self):
         return self.w.attn_flops(self.window)
@@ -408,6 +462,8 @@ def main():
                          "pkv_reposition_splice_freqs (M-RoPE temporal move, Llama-3.1 scaling)")
     ap.add_argument("--window", type=int, default=0,
                     help="sliding-window attention over the full cache (0 = causal; single-sequence workloads)")
+    ap.add_argument("--paged", type=int, default=0,
+                    help="page size of a paged KV cache (0 = contiguous cache)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -430,7 +486,7 @@ def main():
         step = BatchedStep(w, args.splits)
     else:
         w = synth.WORKLOADS[args.workload]
-        step = GqaStep(w, args.splits, window=args.window, rope=args.rope)
+        step = GqaStep(w, args.splits, window=args.window, rope=args.rope, page_size=args.paged)
     log("workload", w)
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream

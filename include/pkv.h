@@ -150,6 +150,40 @@ pkv_status pkv_reposition_splice_freqs(const void* src_k, const void* src_v, voi
                                        const double* omega, int32_t rope_dim, const pkv_layout* layout,
                                        void* stream);
 
+/* Paged KV cache (Sec. 8: paged attention keeps per-token KV, so the
+ * operations apply unchanged; vLLM serving).  Sequence s's logical slot p
+ * lives in physical page block_table[s * max_pages + p / page_size] at
+ * in-page slot p % page_size.  K element (layer l, kv head h, page P, in-page
+ * slot o, channel c) is at l*stride[0] + h*stride[1] + P*page_stride_k +
+ * o*stride[2] + c, with stride[] the {layer, head, slot} element strides of
+ * the layout / descriptor passed alongside (V likewise with page_stride_v).
+ * A pool laid out [layer][page][slot][kv_head][d] has stride = {n_pages *
+ * page_size * Hkv * d, d, Hkv * d} and page_stride = page_size * Hkv * d. */
+typedef struct pkv_paged_cache {
+    int32_t page_size;           /* slots per page: a power of two, 32 .. 2^20 */
+    int32_t max_pages;           /* block_table entries per sequence */
+    const int32_t* block_table;  /* device int32 [n_seqs][max_pages] */
+    int64_t n_pages;             /* physical pages in the pool */
+    int64_t page_stride_k;       /* elements between consecutive physical pages of K */
+    int64_t page_stride_v;       /* ... of V (unused when there is no V tensor) */
+} pkv_paged_cache;
+
+/* Reposition + splice into a paged destination cache: as pkv_reposition_splice
+ * with the destination slot dst_pos[t] taken as a logical slot of the sequence
+ * whose block table is row 0 of paging->block_table.  layout->dst_capacity is
+ * the logical capacity (at most max_pages * page_size) and the dst strides are
+ * {layer, head, in-page slot}.  A token whose slot or page entry is out of
+ * range is skipped (and *err_flag set).  The source is a contiguous chunk as
+ * in pkv_reposition_splice.
+ * Errors: as pkv_reposition_splice; PKV_ERR_NULL (paging or its block table),
+ * PKV_ERR_SHAPE (page_size not a power of two in [32, 2^20], non-positive
+ * max_pages / n_pages, n_pages beyond 2^31 - 1, negative page strides, dst_capacity beyond
+ * max_pages * page_size), PKV_ERR_ALIGN (page strides not 16-byte multiples). */
+pkv_status pkv_reposition_splice_paged(const void* src_k, const void* src_v, void* dst_k, void* dst_v,
+                                       const int32_t* src_pos, const int32_t* dst_pos, float rope_theta,
+                                       int32_t rope_dim, const pkv_layout* layout,
+                                       const pkv_paged_cache* paging, void* stream);
+
 /* One chunk of a multi-chunk composition (Sec. 5: a library of skills
  * composes; Sec. 7 E4: memory split into independently precompiled blocks).
  * Source tokens src_slot0 .. src_slot0+n_tokens-1 were encoded at positions
@@ -248,6 +282,22 @@ pkv_status pkv_suffix_attention(const void* q, const void* k_cache, const void* 
                                 int32_t n_kv_heads, int32_t head_dim, float scale,
                                 const pkv_attn_desc* desc, void* workspace, size_t workspace_bytes,
                                 void* stream);
+
+/* Suffix attention over a paged cache: as pkv_suffix_attention with sequence
+ * s's slots read through row s of paging->block_table (desc->kv_base must be
+ * NULL; desc->cache_slots is the logical capacity, at most max_pages *
+ * page_size; k/v strides are {layer, head, in-page slot}).  A 32-key tile
+ * always lies within one page.  Block-table entries outside [0, n_pages) are
+ * clamped so that every read stays inside the pool (the slots they map are then
+ * undefined).  bf16 only (GQA and MLA).
+ * Errors: as pkv_suffix_attention; PKV_ERR_NULL (paging, block table),
+ * PKV_ERR_SHAPE (paging fields as for the paged splice, kv_base given),
+ * PKV_ERR_UNSUPPORTED (fp32). */
+pkv_status pkv_suffix_attention_paged(const void* q, const void* k_pages, const void* v_pages, void* out,
+                                      const int32_t* q_pos, const int32_t* kv_len, int32_t n_q_heads,
+                                      int32_t n_kv_heads, int32_t head_dim, float scale,
+                                      const pkv_attn_desc* desc, const pkv_paged_cache* paging,
+                                      void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Diagnostics

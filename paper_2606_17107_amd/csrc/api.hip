@@ -56,10 +56,43 @@ pkv_status device_status(hipError_t e, const char* what) {
     return fail(PKV_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
 }
 
+// Validation of a paged-cache descriptor serving `logical_slots` slots per
+// sequence with elements of `eb` bytes; sets *shift to log2(page_size).
+pkv_status check_paging(const pkv_paged_cache* pg, int64_t logical_slots, int eb, int* shift) {
+    if (!pg) return fail(PKV_ERR_NULL, "paging is NULL");
+    if (!pg->block_table) return fail(PKV_ERR_NULL, "paging.block_table is NULL");
+    const int32_t b = pg->page_size;
+    if (b < 32 || b > (1 << 20) || (b & (b - 1)))
+        return fail(PKV_ERR_SHAPE, "page_size %d must be a power of two in [32, 2^20]", b);
+    if (pg->max_pages <= 0 || pg->n_pages <= 0 || pg->n_pages > 0x7fffffff)
+        return fail(PKV_ERR_SHAPE, "max_pages (%d) and n_pages (%lld) must be positive (n_pages < 2^31)",
+                    pg->max_pages, (long long)pg->n_pages);
+    if (pg->page_stride_k < 0 || pg->page_stride_v < 0)
+        return fail(PKV_ERR_SHAPE, "page strides must be non-negative");
+    if ((pg->page_stride_k * eb) % 16 || (pg->page_stride_v * eb) % 16)
+        return fail(PKV_ERR_ALIGN, "page strides must be multiples of 16 bytes");
+    if (logical_slots > (int64_t)pg->max_pages * b)
+        return fail(PKV_ERR_SHAPE, "%lld logical slots exceed max_pages * page_size = %lld",
+                    (long long)logical_slots, (long long)pg->max_pages * b);
+    int sh = 0;
+    while ((1 << sh) < b) ++sh;
+    *shift = sh;
+    return PKV_OK;
+}
+
+// Byte range of a paged pool: {layer, head, page, in-page slot} with strides
+// {stride[0], stride[1], page_stride, stride[2]}.
+Range paged_extent(const void* p, const int64_t* stride, int64_t page_stride, int64_t n_layers, int64_t n_heads,
+                   const pkv_paged_cache* pg, int64_t row_elems, int eb) {
+    const int64_t st[4] = {stride[0], stride[1], page_stride, stride[2]};
+    const int64_t cnt[4] = {n_layers, n_heads, pg->n_pages, pg->page_size};
+    return extent(p, st, cnt, 4, row_elems, eb);
+}
+
 // Shared validation of reposition+splice arguments.  Fills `a` on success.
 pkv_status check_splice(const void* src_k, const void* src_v, void* dst_k, void* dst_v,
                         float rope_theta, int32_t rope_dim, const pkv_layout* L, bool allow_inplace,
-                        pkv::SpliceArgs& a) {
+                        pkv::SpliceArgs& a, const pkv_paged_cache* pg = nullptr) {
     if (!L) return fail(PKV_ERR_NULL, "layout is NULL");
     if (!src_k || !dst_k) return fail(PKV_ERR_NULL, "src_k and dst_k are required");
     if (L->dtype != PKV_BF16 && L->dtype != PKV_F32)
@@ -116,6 +149,14 @@ pkv_status check_splice(const void* src_k, const void* src_v, void* dst_k, void*
     Range sv = extent(src_v, L->src_v_stride, src_cnt, 3, L->v_dim, eb);
     Range dk = extent(dst_k, L->dst_k_stride, dst_cnt, 3, L->head_dim, eb);
     Range dv = extent(dst_v, L->dst_v_stride, dst_cnt, 3, L->v_dim, eb);
+    int page_shift = 0;
+    if (pg) {
+        pkv_status st = check_paging(pg, L->dst_capacity, eb, &page_shift);
+        if (st != PKV_OK) return st;
+        dk = paged_extent(dst_k, L->dst_k_stride, pg->page_stride_k, L->n_layers, L->n_kv_heads, pg, L->head_dim, eb);
+        dv = paged_extent(dst_v, L->dst_v_stride, pg->page_stride_v, L->n_layers, L->n_kv_heads, pg, L->v_dim, eb);
+        allow_inplace = false;
+    }
     const bool k_inplace = allow_inplace && src_k == dst_k &&
                            memcmp(L->src_k_stride, L->dst_k_stride, sizeof L->src_k_stride) == 0;
     const bool v_inplace = allow_inplace && src_v && src_v == dst_v &&
@@ -148,6 +189,14 @@ pkv_status check_splice(const void* src_k, const void* src_v, void* dst_k, void*
         a.dst_v_stride[i] = L->dst_v_stride[i];
     }
     a.err_flag = L->err_flag;
+    if (pg) {
+        a.dst_pages = pg->block_table;
+        a.page_shift = page_shift;
+        a.max_pages = pg->max_pages;
+        a.n_pages = pg->n_pages;
+        a.dst_k_page_stride = pg->page_stride_k;
+        a.dst_v_page_stride = pg->page_stride_v;
+    }
     return PKV_OK;
 }
 
@@ -155,7 +204,7 @@ pkv_status check_splice(const void* src_k, const void* src_v, void* dst_k, void*
 pkv_status check_attention(const void* q, const void* k, const void* v, void* out,
                            const int32_t* q_pos, const int32_t* kv_len, int32_t H, int32_t Hkv,
                            int32_t D, float scale, const pkv_attn_desc* d, bool check_alias,
-                           pkv::AttnArgs& a) {
+                           pkv::AttnArgs& a, const pkv_paged_cache* pg = nullptr) {
     if (!d) return fail(PKV_ERR_NULL, "desc is NULL");
     if (!q || !k || !v || !out || !q_pos || !kv_len)
         return fail(PKV_ERR_NULL, "q, k_cache, v_cache, out, q_pos and kv_len are required");
@@ -193,6 +242,16 @@ pkv_status check_attention(const void* q, const void* k, const void* v, void* ou
             (d->o_stride[i] * eb) % 16)
             return fail(PKV_ERR_ALIGN, "strides must be multiples of 16 bytes");
     }
+    int page_shift = 0;
+    if (pg) {
+        if (d->dtype != PKV_BF16) return fail(PKV_ERR_UNSUPPORTED, "paged attention is bf16 only");
+        if (d->kv_base) return fail(PKV_ERR_SHAPE, "desc.kv_base must be NULL for a paged cache");
+        pkv_status st = check_paging(pg, d->cache_slots, eb, &page_shift);
+        if (st != PKV_OK) return st;
+        if (d->variant == PKV_ATTN_MLA && pg->page_stride_v != pg->page_stride_k)
+            return fail(PKV_ERR_SHAPE, "MLA reads values from the latent channels: page_stride_v must equal "
+                                       "page_stride_k");
+    }
     // out must not overlap any input
     if (check_alias && d->total_q > 0) {
         const int64_t oc[3] = {d->n_layers, d->total_q, H};
@@ -203,6 +262,10 @@ pkv_status check_attention(const void* q, const void* k, const void* v, void* ou
         Range rq = extent(q, d->q_stride, qc, 3, D, eb);
         Range rk = extent(k, d->k_stride, kc, 3, D, eb);
         Range rv = extent(v, d->v_stride, kc, 3, d->head_dim_v, eb);
+        if (pg) {
+            rk = paged_extent(k, d->k_stride, pg->page_stride_k, d->n_layers, Hkv, pg, D, eb);
+            rv = paged_extent(v, d->v_stride, pg->page_stride_v, d->n_layers, Hkv, pg, d->head_dim_v, eb);
+        }
         if (overlap(ro, rq) || overlap(ro, rk) || overlap(ro, rv))
             return fail(PKV_ERR_ALIAS, "out overlaps an input tensor");
     }
@@ -236,6 +299,14 @@ pkv_status check_attention(const void* q, const void* k, const void* v, void* ou
         a.k_stride[i] = d->k_stride[i];
         a.v_stride[i] = d->v_stride[i];
         a.o_stride[i] = d->o_stride[i];
+    }
+    if (pg) {
+        a.block_table = pg->block_table;
+        a.page_shift = page_shift;
+        a.max_pages = pg->max_pages;
+        a.n_pages = pg->n_pages;
+        a.k_page_stride = pg->page_stride_k;
+        a.v_page_stride = pg->page_stride_v;
     }
     return PKV_OK;
 }
@@ -273,6 +344,21 @@ PKV_EXPORT pkv_status pkv_reposition_splice_freqs(const void* src_k, const void*
     a.omega = omega;
     if (a.n_tokens == 0) return ok();
     return device_status(pkv::launch_splice(a, (hipStream_t)stream), "reposition_splice_freqs launch");
+}
+
+PKV_EXPORT pkv_status pkv_reposition_splice_paged(const void* src_k, const void* src_v, void* dst_k,
+                                                  void* dst_v, const int32_t* src_pos, const int32_t* dst_pos,
+                                                  float rope_theta, int32_t rope_dim, const pkv_layout* layout,
+                                                  const pkv_paged_cache* paging, void* stream) {
+    pkv::SpliceArgs a;
+    if (!paging) return fail(PKV_ERR_NULL, "paging is NULL");
+    pkv_status st = check_splice(src_k, src_v, dst_k, dst_v, rope_theta, rope_dim, layout, false, a, paging);
+    if (st != PKV_OK) return st;
+    if (!src_pos || !dst_pos) return fail(PKV_ERR_NULL, "src_pos and dst_pos are required");
+    a.src_pos = src_pos;
+    a.dst_pos = dst_pos;
+    if (a.n_tokens == 0) return ok();
+    return device_status(pkv::launch_splice(a, (hipStream_t)stream), "reposition_splice_paged launch");
 }
 
 PKV_EXPORT pkv_status pkv_reposition_splice_batched(const void* src_k, const void* src_v, void* dst_k,
@@ -313,14 +399,15 @@ PKV_EXPORT size_t pkv_attention_workspace_size(const pkv_attn_desc* desc, int32_
     return pkv::attention_workspace_bytes(a, pkv::attention_splits(a));
 }
 
-PKV_EXPORT pkv_status pkv_suffix_attention(const void* q, const void* k_cache, const void* v_cache,
-                                           void* out, const int32_t* q_pos, const int32_t* kv_len,
-                                           int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
-                                           float scale, const pkv_attn_desc* desc, void* workspace,
-                                           size_t workspace_bytes, void* stream) {
+namespace {
+
+pkv_status run_attention(const void* q, const void* k_cache, const void* v_cache, void* out, const int32_t* q_pos,
+                         const int32_t* kv_len, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, float scale,
+                         const pkv_attn_desc* desc, const pkv_paged_cache* paging, void* workspace,
+                         size_t workspace_bytes, void* stream) {
     pkv::AttnArgs a;
     pkv_status st = check_attention(q, k_cache, v_cache, out, q_pos, kv_len, n_q_heads, n_kv_heads,
-                                    head_dim, scale, desc, true, a);
+                                    head_dim, scale, desc, true, a, paging);
     if (st != PKV_OK) return st;
     const int splits = pkv::attention_splits(a);
     const size_t need = pkv::attention_workspace_bytes(a, splits);
@@ -339,6 +426,28 @@ PKV_EXPORT pkv_status pkv_suffix_attention(const void* q, const void* k_cache, c
     }
     if (a.total_q == 0) return ok();
     return device_status(pkv::launch_attention(a, (hipStream_t)stream), "suffix_attention launch");
+}
+
+}  // namespace
+
+PKV_EXPORT pkv_status pkv_suffix_attention(const void* q, const void* k_cache, const void* v_cache,
+                                           void* out, const int32_t* q_pos, const int32_t* kv_len,
+                                           int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                           float scale, const pkv_attn_desc* desc, void* workspace,
+                                           size_t workspace_bytes, void* stream) {
+    return run_attention(q, k_cache, v_cache, out, q_pos, kv_len, n_q_heads, n_kv_heads, head_dim, scale, desc,
+                         nullptr, workspace, workspace_bytes, stream);
+}
+
+PKV_EXPORT pkv_status pkv_suffix_attention_paged(const void* q, const void* k_pages, const void* v_pages,
+                                                 void* out, const int32_t* q_pos, const int32_t* kv_len,
+                                                 int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                                 float scale, const pkv_attn_desc* desc,
+                                                 const pkv_paged_cache* paging, void* workspace,
+                                                 size_t workspace_bytes, void* stream) {
+    if (!paging) return fail(PKV_ERR_NULL, "paging is NULL");
+    return run_attention(q, k_pages, v_pages, out, q_pos, kv_len, n_q_heads, n_kv_heads, head_dim, scale, desc,
+                         paging, workspace, workspace_bytes, stream);
 }
 
 PKV_EXPORT const char* pkv_last_error(void) { return g_err; }

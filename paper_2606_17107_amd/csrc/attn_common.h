@@ -76,6 +76,53 @@ __device__ inline SeqInfo seq_info(const AttnArgs& a, int seq) {
     return s;
 }
 
+// Paged caches: the block-table row of one sequence seen through a window of
+// 256 consecutive entries held by the wave, four registers of 64 lanes (lane
+// l of register r holds entry w0 + 64 r + l).  Tiles are visited in ascending
+// order, so the window moves forward a whole window at a time; each entry is
+// clamped into the pool when loaded, so every tile read stays inside it.
+struct PageWindow {
+    const int32_t* row;   // block_table + seq * max_pages
+    int n_entries;        // max_pages
+    int last_page;        // n_pages - 1
+    int w0;               // first entry in the window
+    int id0, id1, id2, id3;   // four registers, not an array: no indexed private memory
+
+    __device__ __forceinline__ int entry(int e) const {
+        const int v = e < n_entries ? row[e] : 0;
+        return min(max(v, 0), last_page);
+    }
+    __device__ __forceinline__ void load(int first) {
+        w0 = first;
+        const int l = first + (int)__lane_id();
+        id0 = entry(l);
+        id1 = entry(l + 64);
+        id2 = entry(l + 128);
+        id3 = entry(l + 192);
+    }
+    __device__ __forceinline__ void init(const AttnArgs& a, int seq, int first_entry) {
+        row = a.block_table + (int64_t)seq * a.max_pages;
+        n_entries = a.max_pages;
+        last_page = (int)(a.n_pages - 1);
+        load(first_entry);
+    }
+    // Element offset of logical slot t0 (the first key of a tile, which lies
+    // in one page) from the pool's (layer, head) origin.
+    __device__ __forceinline__ int64_t offset(const AttnArgs& a, int t0, int64_t page_stride, int64_t slot_stride) {
+        const int e = t0 >> a.page_shift;
+        if ((unsigned)(e - w0) >= 256u) load(e);
+        const int rel = e - w0;
+        // Read the lane from each register and select among the scalars: a
+        // select among the registers would be folded into an indexed access of
+        // the struct, which then cannot live in registers.
+        const int r = rel >> 6, l = rel & 63;
+        const int p0 = __builtin_amdgcn_readlane(id0, l), p1 = __builtin_amdgcn_readlane(id1, l);
+        const int p2 = __builtin_amdgcn_readlane(id2, l), p3 = __builtin_amdgcn_readlane(id3, l);
+        const int page = r == 0 ? p0 : r == 1 ? p1 : r == 2 ? p2 : p3;
+        return (int64_t)page * page_stride + (int64_t)(t0 & ((1 << a.page_shift) - 1)) * slot_stride;
+    }
+};
+
 __device__ inline int wave_max_i(int v) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) v = max(v, __shfl_xor(v, o));

@@ -56,7 +56,7 @@ __device__ inline int swz_v(int key) {
     else return ((key & 3) << 1) | ((key >> 2) & 1);
 }
 
-template <int D, int QB, int NW, int NS, bool PIPE>
+template <int D, int QB, int NW, int NS, bool PIPE, bool PAGED>
 __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, Plan p) {
     constexpr int CH = D / 8;              // 16-byte chunks per row
     constexpr int BN = PIPE ? 32 : 64;     // keys per tile
@@ -183,8 +183,17 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
     }
     // Stage the tile starting at key t0.  A tile that runs past the last
     // visible key re-reads that key for the missing rows (masked later).
+    // Paged cache: tiles start on a multiple of BN, which divides the page
+    // size, so each tile lies in one page.
+    PageWindow pw;
+    if constexpr (PAGED) pw.init(a, seq, k_begin >> a.page_shift);
+    const int64_t tpage = (wave_v ? a.v_page_stride : a.k_page_stride) * 2;   // bytes between pages
     auto issue = [&](int t0, uint16_t* ks_dst, uint16_t* vs_dst) __attribute__((always_inline)) {
-        const char* tile = tens + (int64_t)t0 * trow;
+        const char* tile;
+        if constexpr (PAGED)
+            tile = tens + pw.offset(a, t0, tpage, trow);
+        else
+            tile = tens + (int64_t)t0 * trow;
         const uint32_t lds0 = lds_addr_of((wave_v ? vs_dst : ks_dst) + blk0 * 64 * 8);
         if (t0 + BN <= loop_end) {
 #pragma unroll
@@ -696,13 +705,13 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
 // Kernel shapes (Plan.ns): 4 waves x 32 rows, two workgroups per CU, and
 //   ns == 4: 32-key tiles, software-pipelined (64 KB of LDS stages);
 //   ns == 2: 64-key tiles, plain order (64 KB of LDS stages).
-template <int D>
+template <int D, bool PAGED>
 hipError_t launch_d(const AttnArgs& a, const Plan& p, dim3 grid, hipStream_t stream) {
     if (p.nw != 4 || p.qb != 1) return hipErrorInvalidValue;
     if (p.ns == 4)
-        hipLaunchKernelGGL((attn_gqa_bf16_kernel<D, 1, 4, 4, true>), grid, dim3(256), 0, stream, a, p);
-    else if (p.ns == 2)
-        hipLaunchKernelGGL((attn_gqa_bf16_kernel<D, 1, 4, 2, false>), grid, dim3(256), 0, stream, a, p);
+        hipLaunchKernelGGL((attn_gqa_bf16_kernel<D, 1, 4, 4, true, PAGED>), grid, dim3(256), 0, stream, a, p);
+    else if (p.ns == 2 && (!PAGED || a.page_shift >= 6))   // 64-key tiles need pages of 64 slots or more
+        hipLaunchKernelGGL((attn_gqa_bf16_kernel<D, 1, 4, 2, false, PAGED>), grid, dim3(256), 0, stream, a, p);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();
@@ -711,8 +720,12 @@ hipError_t launch_d(const AttnArgs& a, const Plan& p, dim3 grid, hipStream_t str
 }  // namespace
 
 hipError_t launch_attn_gqa_bf16(const AttnArgs& a, const Plan& p, dim3 grid, hipStream_t stream) {
-    if (a.head_dim == 64) return launch_d<64>(a, p, grid, stream);
-    return launch_d<128>(a, p, grid, stream);
+    if (a.block_table) {
+        if (a.head_dim == 64) return launch_d<64, true>(a, p, grid, stream);
+        return launch_d<128, true>(a, p, grid, stream);
+    }
+    if (a.head_dim == 64) return launch_d<64, false>(a, p, grid, stream);
+    return launch_d<128, false>(a, p, grid, stream);
 }
 
 }  // namespace pkv

@@ -51,7 +51,7 @@ constexpr int MCH = DQK / 8;   // 16-byte chunks per row: 72
 // the other half of its 8-chunk group.
 __device__ inline int mswz(int key) { return (((key >> 1) & 1) << 2) | ((key >> 2) & 3); }
 
-template <int NS, int NW>
+template <int NS, int NW, bool PAGED>
 __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs a, Plan p) {
     constexpr int NBLK = MBN * MCH / 64;       // 64-lane LDS-DMA blocks per tile: 36
     constexpr int PER = (NBLK + NW - 1) / NW;  // blocks of the busiest wave per tile
@@ -145,8 +145,15 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
         const int logical = (slot % MCH) ^ mswz(key_of[i]);
         src_off[i] = (int32_t)((int64_t)key_of[i] * kss * 2 + logical * 16);
     }
+    // Paged cache: a 32-key tile lies in one page (page sizes are multiples of 32).
+    PageWindow pw;
+    if constexpr (PAGED) pw.init(a, seq, k_begin >> a.page_shift);
     auto issue = [&](int t0, uint16_t* dst_stage) {
-        const char* kt = (const char*)(kbase + (int64_t)t0 * kss);
+        const char* kt;
+        if constexpr (PAGED)
+            kt = (const char*)(kbase + pw.offset(a, t0, a.k_page_stride, kss));
+        else
+            kt = (const char*)(kbase + (int64_t)t0 * kss);
         const uint32_t lds0 = lds_addr_of(dst_stage + wave * 64 * 8);
         const bool full = t0 + MBN <= loop_end;
 #pragma unroll
@@ -373,8 +380,12 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
 
 hipError_t launch_attn_mla_bf16(const AttnArgs& a, const Plan& p, dim3 grid, hipStream_t stream) {
     if (p.nw != PKV_MLA_WAVES || p.ns != PKV_MLA_STAGES || p.BM != PKV_MLA_WAVES / 2 * 32) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((attn_mla_bf16_kernel<PKV_MLA_STAGES, PKV_MLA_WAVES>), grid, dim3(PKV_MLA_WAVES * 64), 0, stream,
-                       a, p);
+    if (a.block_table)
+        hipLaunchKernelGGL((attn_mla_bf16_kernel<PKV_MLA_STAGES, PKV_MLA_WAVES, true>), grid,
+                           dim3(PKV_MLA_WAVES * 64), 0, stream, a, p);
+    else
+        hipLaunchKernelGGL((attn_mla_bf16_kernel<PKV_MLA_STAGES, PKV_MLA_WAVES, false>), grid,
+                           dim3(PKV_MLA_WAVES * 64), 0, stream, a, p);
     return hipGetLastError();
 }
 

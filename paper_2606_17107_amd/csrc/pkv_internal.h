@@ -49,6 +49,14 @@ struct SpliceArgs {
     int64_t dst_k_stride[3];
     int64_t dst_v_stride[3];
     int32_t* err_flag;
+    // paged destination (per-token mode): logical slot p -> page
+    // dst_pages[p >> page_shift], in-page slot p & (page_size - 1)
+    const int32_t* dst_pages;  // null: contiguous destination
+    int32_t page_shift;
+    int32_t max_pages;
+    int64_t n_pages;
+    int64_t dst_k_page_stride;  // elements
+    int64_t dst_v_page_stride;
 };
 
 hipError_t launch_splice(const SpliceArgs& a, hipStream_t stream);
@@ -86,6 +94,14 @@ struct AttnArgs {
     int64_t k_stride[3];
     int64_t v_stride[3];
     int64_t o_stride[3];
+    // paged cache: sequence s's slot p is in page block_table[s * max_pages +
+    // (p >> page_shift)], in-page slot p & (page_size - 1)
+    const int32_t* block_table;  // null: contiguous cache
+    int32_t page_shift;
+    int32_t max_pages;
+    int64_t n_pages;
+    int64_t k_page_stride;       // elements
+    int64_t v_page_stride;
 };
 
 // Split plan shared by the workspace query and the launcher.

@@ -217,8 +217,9 @@ __device__ inline int lane_pair(int l, int j, int half_r) {
         return j < CE / 2 ? l * (CE / 2) + j : (half_r + l) * (CE / 2) + (j - CE / 2);
 }
 
-template <int EB, int STYLE, bool SEG, bool TAB>
+template <int EB, int STYLE, bool SEG, bool TAB, bool PAGED>
 __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, FreqArg<TAB> ft) {
+    static_assert(!(PAGED && SEG), "paged destinations are per-token mode only");
     constexpr int CE = 16 / EB;   // elements per 16-byte chunk = pairs per rotary lane
     // Explicit frequencies: lane l holds those of pairs l and 64 + l, loaded
     // before anything else so that waiting for them leaves the later loads in
@@ -273,6 +274,7 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
     const int64_t d0 = is_k ? a.dst_k_stride[0] : a.dst_v_stride[0];
     const int64_t d1 = is_k ? a.dst_k_stride[1] : a.dst_v_stride[1];
     const int64_t d2 = is_k ? a.dst_k_stride[2] : a.dst_v_stride[2];
+    const int64_t dpg = PAGED ? (is_k ? a.dst_k_page_stride : a.dst_v_page_stride) : 0;
     const char* const src_t = (is_k ? a.src_k : a.src_v) + ca * 16;
     char* const dst_t = (is_k ? a.dst_k : a.dst_v) + ca * 16;
     const int ob = (cb - ca) * 16;
@@ -356,6 +358,19 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
         }
         const bool valid = dst_slot >= 0 && dst_slot < a.dst_capacity;
         const bool work = active && valid;
+        // Paged destination: the slot's page id is read from an in-range entry
+        // for every lane (no branch, so the wait for it stays with the K/V
+        // wait before the stores); a page outside the pool skips the token.
+        int64_t dst_row = dst_slot;
+        bool page_ok = true;
+        if constexpr (PAGED) {
+            const int64_t pidx = work ? dst_slot >> a.page_shift : 0;
+            const int32_t page = a.dst_pages[pidx];
+            page_ok = page >= 0 && page < a.n_pages;
+            dst_row = (int64_t)page * dpg + (dst_slot & ((1 << a.page_shift) - 1)) * d2;
+        } else {
+            dst_row = dst_slot * d2;
+        }
 
         // Rotation coefficients.  When every working lane of the wave has the
         // same delta (always so in segment mode; so for a contiguous chunk in
@@ -400,8 +415,8 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
         }
         rot = rope && delta != 0;
 
-        if (work) {
-            char* dbase = dst_t + dst_slot * d2 * EB;
+        if (work && page_ok) {
+            char* dbase = dst_t + dst_row * EB;
             for (int r = r0;;) {
 #pragma unroll
                 for (int u = 0; u < kUnroll; ++u) {
@@ -416,26 +431,30 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
                 load_rows(r);
             }
         }
-        if (present && !work && lane == 0 && grp == 0 && a.err_flag) atomicOr(a.err_flag, 1);
+        if (present && !(work && page_ok) && lane == 0 && grp == 0 && a.err_flag) atomicOr(a.err_flag, 1);
         if constexpr (!SEG) break;
     }
 }
 
 template <int EB, int STYLE>
 hipError_t launch_typed(const SpliceArgs& a, const Geo& g, dim3 grid, dim3 block, hipStream_t st) {
-    if (a.omega) {
+    if (a.dst_pages) {   // paged destination: per-token mode, theta schedule
+        if (a.segs || a.omega) return hipErrorInvalidValue;
+        const FreqArg<false> ft;
+        hipLaunchKernelGGL((splice_kernel<EB, STYLE, false, false, true>), grid, block, 0, st, a, g, ft);
+    } else if (a.omega) {
         FreqArg<true> ft;
         for (int i = 0; i < (1 << kPairBits); ++i) ft.w[i] = i < g.n_pairs ? a.omega[i] : 0.0;
         if (a.segs)
-            hipLaunchKernelGGL((splice_kernel<EB, STYLE, true, true>), grid, block, 0, st, a, g, ft);
+            hipLaunchKernelGGL((splice_kernel<EB, STYLE, true, true, false>), grid, block, 0, st, a, g, ft);
         else
-            hipLaunchKernelGGL((splice_kernel<EB, STYLE, false, true>), grid, block, 0, st, a, g, ft);
+            hipLaunchKernelGGL((splice_kernel<EB, STYLE, false, true, false>), grid, block, 0, st, a, g, ft);
     } else {
         const FreqArg<false> ft;
         if (a.segs)
-            hipLaunchKernelGGL((splice_kernel<EB, STYLE, true, false>), grid, block, 0, st, a, g, ft);
+            hipLaunchKernelGGL((splice_kernel<EB, STYLE, true, false, false>), grid, block, 0, st, a, g, ft);
         else
-            hipLaunchKernelGGL((splice_kernel<EB, STYLE, false, false>), grid, block, 0, st, a, g, ft);
+            hipLaunchKernelGGL((splice_kernel<EB, STYLE, false, false, false>), grid, block, 0, st, a, g, ft);
     }
     return hipGetLastError();
 }
@@ -460,6 +479,9 @@ hipError_t launch_splice(const SpliceArgs& a, hipStream_t stream) {
     // Every index array the kernel dereferences must be present.
     if (!a.src_k || !a.dst_k || (g.lanes_v > 0 && (!a.src_v || !a.dst_v)) ||
         (!seg && (!a.src_pos || !a.dst_pos)))
+        return hipErrorInvalidValue;
+    if (a.dst_pages && (a.page_shift < 5 || a.page_shift > 20 || a.n_pages <= 0 ||
+                        a.dst_capacity > ((int64_t)a.max_pages << a.page_shift)))
         return hipErrorInvalidValue;
     const int64_t tokens = seg ? a.max_seg_tokens : a.n_tokens;
     const int64_t nz = seg ? a.n_segs : 1;

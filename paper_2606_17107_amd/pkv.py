@@ -65,8 +65,16 @@ class pkv_attn_desc(ctypes.Structure):
     ]
 
 
-SYMBOLS = ("pkv_reposition_splice", "pkv_reposition_splice_freqs", "pkv_reposition_splice_batched",
-           "pkv_attention_workspace_size", "pkv_suffix_attention", "pkv_last_error", "pkv_version")
+class pkv_paged_cache(ctypes.Structure):
+    _fields_ = [
+        ("page_size", ctypes.c_int32), ("max_pages", ctypes.c_int32), ("block_table", ctypes.c_void_p),
+        ("n_pages", ctypes.c_int64), ("page_stride_k", ctypes.c_int64), ("page_stride_v", ctypes.c_int64),
+    ]
+
+
+SYMBOLS = ("pkv_reposition_splice", "pkv_reposition_splice_freqs", "pkv_reposition_splice_paged",
+           "pkv_reposition_splice_batched", "pkv_attention_workspace_size", "pkv_suffix_attention",
+           "pkv_suffix_attention_paged", "pkv_last_error", "pkv_version")
 
 _lib = None
 
@@ -93,6 +101,9 @@ def lib() -> ctypes.CDLL:
     L.pkv_reposition_splice_freqs.restype = ctypes.c_int
     L.pkv_reposition_splice_freqs.argtypes = [P, P, P, P, P, P, P, ctypes.POINTER(ctypes.c_double),
                                               ctypes.c_int32, ctypes.POINTER(pkv_layout), P]
+    L.pkv_reposition_splice_paged.restype = ctypes.c_int
+    L.pkv_reposition_splice_paged.argtypes = [P, P, P, P, P, P, ctypes.c_float, ctypes.c_int32,
+                                              ctypes.POINTER(pkv_layout), ctypes.POINTER(pkv_paged_cache), P]
     L.pkv_reposition_splice_batched.restype = ctypes.c_int
     L.pkv_reposition_splice_batched.argtypes = [P, P, P, P, P, ctypes.c_int32, ctypes.c_int32,
                                                 ctypes.c_float, ctypes.c_int32, ctypes.POINTER(pkv_layout), P]
@@ -102,6 +113,10 @@ def lib() -> ctypes.CDLL:
     L.pkv_suffix_attention.restype = ctypes.c_int
     L.pkv_suffix_attention.argtypes = [P, P, P, P, P, P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                        ctypes.c_float, ctypes.POINTER(pkv_attn_desc), P, ctypes.c_size_t, P]
+    L.pkv_suffix_attention_paged.restype = ctypes.c_int
+    L.pkv_suffix_attention_paged.argtypes = [P, P, P, P, P, P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                             ctypes.c_float, ctypes.POINTER(pkv_attn_desc),
+                                             ctypes.POINTER(pkv_paged_cache), P, ctypes.c_size_t, P]
     L.pkv_last_error.restype = ctypes.c_char_p
     L.pkv_last_error.argtypes = []
     L.pkv_version.restype = ctypes.c_int32
@@ -150,6 +165,14 @@ def pkv_reposition_splice_freqs(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, ds
                                              ctypes.byref(layout) if layout is not None else None, _stream(stream))
 
 
+def pkv_reposition_splice_paged(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, rope_theta, rope_dim, layout, paging,
+                                stream=None) -> int:
+    return lib().pkv_reposition_splice_paged(_ptr(src_k), _ptr(src_v), _ptr(dst_k), _ptr(dst_v), _ptr(src_pos),
+                                             _ptr(dst_pos), float(rope_theta), int(rope_dim),
+                                             ctypes.byref(layout) if layout is not None else None,
+                                             ctypes.byref(paging) if paging is not None else None, _stream(stream))
+
+
 def pkv_reposition_splice_batched(src_k, src_v, dst_k, dst_v, segs, n_segs, max_seg_tokens, rope_theta,
                                   rope_dim, layout, stream=None) -> int:
     return lib().pkv_reposition_splice_batched(
@@ -169,6 +192,15 @@ def pkv_suffix_attention(q, k_cache, v_cache, out, q_pos, kv_len, n_q_heads, n_k
         _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(out), _ptr(q_pos), _ptr(kv_len), int(n_q_heads),
         int(n_kv_heads), int(head_dim), float(scale), ctypes.byref(desc) if desc is not None else None,
         _ptr(workspace), int(workspace_bytes), _stream(stream))
+
+
+def pkv_suffix_attention_paged(q, k_pages, v_pages, out, q_pos, kv_len, n_q_heads, n_kv_heads, head_dim, scale,
+                               desc, paging, workspace, workspace_bytes, stream=None) -> int:
+    return lib().pkv_suffix_attention_paged(
+        _ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(out), _ptr(q_pos), _ptr(kv_len), int(n_q_heads),
+        int(n_kv_heads), int(head_dim), float(scale), ctypes.byref(desc) if desc is not None else None,
+        ctypes.byref(paging) if paging is not None else None, _ptr(workspace), int(workspace_bytes),
+        _stream(stream))
 
 
 def pkv_last_error() -> str:
@@ -305,3 +337,77 @@ def suffix_attention(q, k_cache, v_cache, out, q_pos, kv_len, scale, max_kv_len,
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
     _check(pkv_suffix_attention(q, k_cache, v_cache, out, q_pos, kv_len, H, Hkv, D, scale, desc,
                                 workspace, need, stream))
+
+
+# ---- paged caches ------------------------------------------------------------
+# Pools are [layer][page][in-page slot][kv_head][channel] (any strides, channels
+# contiguous); a block table is int32 [n_seqs][max_pages] on the device.
+
+def pool_strides3(pool: Optional[torch.Tensor]):
+    """{layer, head, in-page slot} element strides of a 5-D pool."""
+    if pool is None:
+        return _i64x3(0, 0, 0)
+    assert pool.dim() == 5 and pool.stride(4) == 1, "pools are [layer][page][slot][kv_head][channel]"
+    return _i64x3(pool.stride(0), pool.stride(3), pool.stride(2))
+
+
+def make_paging(block_table: torch.Tensor, k_pool: torch.Tensor,
+                v_pool: Optional[torch.Tensor] = None) -> pkv_paged_cache:
+    assert block_table.dtype == torch.int32 and block_table.dim() == 2 and block_table.is_contiguous()
+    pg = pkv_paged_cache()
+    pg.page_size = k_pool.shape[2]
+    pg.max_pages = block_table.shape[1]
+    pg.block_table = block_table.data_ptr()
+    pg.n_pages = k_pool.shape[1]
+    pg.page_stride_k = k_pool.stride(1)
+    pg.page_stride_v = 0 if v_pool is None else v_pool.stride(1)
+    return pg
+
+
+def reposition_splice_paged(src_k, src_v, k_pool, v_pool, src_pos, dst_pos, block_table, rope_theta, rope_dim,
+                            rope_offset=0, rope_style=PKV_ROPE_HALF, dst_capacity=None, err_flag=None,
+                            stream=None) -> None:
+    """Tensor-level call of pkv_reposition_splice_paged: destination slots are logical slots of the
+    sequence whose block-table row is block_table[0]."""
+    L = make_layout(src_k, src_v, src_k, src_v, rope_offset, rope_style, err_flag=err_flag)
+    L.dst_capacity = (block_table.shape[1] * k_pool.shape[2]) if dst_capacity is None else int(dst_capacity)
+    L.dst_k_stride = pool_strides3(k_pool)
+    L.dst_v_stride = pool_strides3(v_pool)
+    pg = make_paging(block_table, k_pool, v_pool)
+    _check(pkv_reposition_splice_paged(src_k, src_v, k_pool, v_pool, src_pos, dst_pos, rope_theta, rope_dim, L, pg,
+                                       stream))
+
+
+def suffix_attention_paged(q, k_pool, v_pool, out, q_pos, kv_len, block_table, scale, max_kv_len, n_seqs=1,
+                           cu_q=None, max_q=None, variant=PKV_ATTN_GQA, n_splits=0, lse_out=None, workspace=None,
+                           stream=None, window=0, cache_slots=None) -> None:
+    """Tensor-level call of pkv_suffix_attention_paged (q [L][rows][H][d], pools as above)."""
+    H = q.shape[2]
+    Hkv = k_pool.shape[3]
+    D = q.shape[3]
+    d = pkv_attn_desc()
+    d.dtype = _dtype_code(q)
+    d.variant = int(variant)
+    d.n_layers = q.shape[0]
+    d.n_seqs = int(n_seqs)
+    d.head_dim_v = out.shape[3]
+    d.total_q = q.shape[1]
+    d.max_q = q.shape[1] if max_q is None else int(max_q)
+    d.max_kv_len = int(max_kv_len)
+    d.n_splits = int(n_splits)
+    d.window = int(window)
+    d.cu_q = None if cu_q is None else cu_q.data_ptr()
+    d.kv_base = None
+    d.cache_slots = block_table.shape[1] * k_pool.shape[2] if cache_slots is None else int(cache_slots)
+    assert q.stride(3) == 1 and out.stride(3) == 1
+    d.q_stride = _i64x3(q.stride(0), q.stride(1), q.stride(2))
+    d.k_stride = pool_strides3(k_pool)
+    d.v_stride = pool_strides3(v_pool)
+    d.o_stride = _i64x3(out.stride(0), out.stride(1), out.stride(2))
+    d.lse_out = None if lse_out is None else lse_out.data_ptr()
+    pg = make_paging(block_table, k_pool, v_pool)
+    need = pkv_attention_workspace_size(d, H, Hkv, D)
+    if need and (workspace is None or workspace.numel() * workspace.element_size() < need):
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    _check(pkv_suffix_attention_paged(q, k_pool, v_pool, out, q_pos, kv_len, H, Hkv, D, scale, d, pg, workspace,
+                                      need, stream))

@@ -39,6 +39,7 @@ def test_struct_sizes_match_header():
     assert ctypes.sizeof(pkv.pkv_segment) == 32
     assert ctypes.sizeof(pkv.pkv_layout) == 40 + 96 + 8
     assert ctypes.sizeof(pkv.pkv_attn_desc) == 40 + 16 + 8 + 96 + 8
+    assert ctypes.sizeof(pkv.pkv_paged_cache) == 8 + 8 + 24
 
 
 BASE = 1 << 40   # fake, 16-byte aligned device addresses; never dereferenced
@@ -189,3 +190,90 @@ def test_freqs_validation():
     assert "omega[7]" in pkv.pkv_last_error()
     assert f(SK, SV, DK, DV, SP, DP, None, w, 127, L, 0) == pkv.PKV_ERR_SHAPE          # odd rope_dim
     assert f(SK, SV, DK + 4096 - 4096 + 8, DV, SP, DP, None, w, 128, L, 0) == pkv.PKV_ERR_ALIGN
+
+
+def good_paging(**kw):
+    pg = pkv.pkv_paged_cache()
+    pg.page_size, pg.max_pages, pg.block_table, pg.n_pages = 32, 4, BASE + 11 * (1 << 32), 8
+    pg.page_stride_k = pg.page_stride_v = 32 * 4 * 128
+    for k, v in kw.items():
+        setattr(pg, k, v)
+    return pg
+
+
+def paged_layout(**kw):
+    # pools [layer 2][page 8][slot 32][kv_head 4][128]
+    pool = pkv._i64x3(8 * 32 * 4 * 128, 128, 4 * 128)
+    L = good_layout(dst_k_stride=pool, dst_v_stride=pool, dst_capacity=128)
+    for k, v in kw.items():
+        setattr(L, k, v)
+    return L
+
+
+@pytest.mark.parametrize("lkw,pkw,args,want", [
+    ({}, None, {}, pkv.PKV_ERR_NULL),
+    ({}, dict(block_table=None), {}, pkv.PKV_ERR_NULL),
+    ({}, dict(page_size=16), {}, pkv.PKV_ERR_SHAPE),
+    ({}, dict(page_size=48), {}, pkv.PKV_ERR_SHAPE),           # not a power of two
+    ({}, dict(page_size=1 << 21), {}, pkv.PKV_ERR_SHAPE),
+    ({}, dict(max_pages=0), {}, pkv.PKV_ERR_SHAPE),
+    ({}, dict(n_pages=0), {}, pkv.PKV_ERR_SHAPE),
+    ({}, dict(n_pages=1 << 31), {}, pkv.PKV_ERR_SHAPE),
+    ({}, dict(page_stride_k=-4096), {}, pkv.PKV_ERR_SHAPE),
+    ({}, dict(page_stride_v=4100), {}, pkv.PKV_ERR_ALIGN),
+    (dict(dst_capacity=129), {}, {}, pkv.PKV_ERR_SHAPE),         # beyond max_pages * page_size
+    ({}, {}, dict(dk=SK + 2048), pkv.PKV_ERR_ALIAS),
+    ({}, {}, dict(dv=DK + 7 * 32 * 4 * 128 * 2), pkv.PKV_ERR_ALIAS),   # V pool starts inside K's last page
+    ({}, {}, dict(sp=None), pkv.PKV_ERR_NULL),
+    ({}, {}, dict(r=127), pkv.PKV_ERR_SHAPE),
+])
+def test_paged_splice_validation(lkw, pkw, args, want):
+    L = paged_layout(**lkw)
+    pg = None if pkw is None else good_paging(**pkw)
+    a = dict(sk=SK, sv=SV, dk=DK, dv=DV, sp=SP, dp=DP, theta=1e4, r=128)
+    a.update(args)
+    st = pkv.pkv_reposition_splice_paged(a["sk"], a["sv"], a["dk"], a["dv"], a["sp"], a["dp"], a["theta"], a["r"],
+                                         L, pg, 0)
+    assert st == want, (st, pkv.pkv_last_error())
+    assert pkv.pkv_last_error()
+
+
+def paged_attn_desc(**kw):
+    pool = pkv._i64x3(8 * 32 * 8 * 128, 128, 8 * 128)   # [layer][page 8][slot 32][kv_head 8][128]
+    d = attn_desc(k_stride=pool, v_stride=pool, cache_slots=128, max_kv_len=128)
+    for k, v in kw.items():
+        setattr(d, k, v)
+    return d
+
+
+def paged_paging(**kw):
+    return good_paging(page_stride_k=32 * 8 * 128, page_stride_v=32 * 8 * 128, **kw)
+
+
+@pytest.mark.parametrize("dkw,pkw,args,want", [
+    ({}, None, {}, pkv.PKV_ERR_NULL),
+    ({}, dict(block_table=None), {}, pkv.PKV_ERR_NULL),
+    ({}, dict(page_size=64 + 32), {}, pkv.PKV_ERR_SHAPE),
+    (dict(dtype=1), {}, {}, pkv.PKV_ERR_UNSUPPORTED),           # paged attention is bf16 only
+    (dict(kv_base=BASE), {}, {}, pkv.PKV_ERR_SHAPE),
+    (dict(cache_slots=129), {}, {}, pkv.PKV_ERR_SHAPE),
+    ({}, {}, dict(o=K + 5 * 32 * 8 * 128 * 2), pkv.PKV_ERR_ALIAS),   # out inside page 5 of the K pool
+    ({}, {}, dict(D=96), pkv.PKV_ERR_UNSUPPORTED),
+    ({}, {}, dict(scale=float("nan")), pkv.PKV_ERR_SHAPE),
+])
+def test_paged_attention_validation(dkw, pkw, args, want):
+    d = paged_attn_desc(**dkw)
+    pg = None if pkw is None else paged_paging(**pkw)
+    a = dict(H=32, Hkv=8, D=128, q=Q, k=K, v=V, o=O, qp=QP, kl=KL, scale=0.08)
+    a.update(args)
+    st = pkv.pkv_suffix_attention_paged(a["q"], a["k"], a["v"], a["o"], a["qp"], a["kl"], a["H"], a["Hkv"], a["D"],
+                                        a["scale"], d, pg, None, 0, 0)
+    assert st == want, (st, pkv.pkv_last_error())
+
+
+def test_paged_mla_page_strides_must_match():
+    pool = pkv._i64x3(8 * 32 * 576, 576, 576)
+    d = attn_desc(variant=1, head_dim_v=512, k_stride=pool, v_stride=pool, cache_slots=128, max_kv_len=128)
+    pg = good_paging(page_stride_k=32 * 576, page_stride_v=32 * 576 + 8)
+    st = pkv.pkv_suffix_attention_paged(Q, K, K, O, QP, KL, 16, 1, 576, 0.07, d, pg, None, 0, 0)
+    assert st == pkv.PKV_ERR_SHAPE and "page_stride_v" in pkv.pkv_last_error()
