@@ -198,16 +198,18 @@ __device__ inline void bare_barrier() {
 }
 
 // Scheduling pattern for a run of N operand loads from LDS, R reads per
-// operand, each operand feeding Q MFMAs: the first two operands' reads go
-// first, then every MFMA group is followed by the reads of the operand two
-// steps ahead.  This bounds the registers held by prefetched operands.
-template <int N, int R, int Q>
+// operand, each operand feeding Q MFMAs: the first A operands' reads go first,
+// then every MFMA group is followed by the reads of the operand A steps ahead.
+// This bounds the registers held by prefetched operands while keeping A LDS
+// round trips in flight.
+template <int N, int R, int Q, int A = 2>
 __device__ inline void sched_reads_mfma() {
-    __builtin_amdgcn_sched_group_barrier(0x100, 2 * R, 0);
+    constexpr int A0 = A < N ? A : N;
+    __builtin_amdgcn_sched_group_barrier(0x100, A0 * R, 0);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, Q, 0);
-        if (i + 2 < N) __builtin_amdgcn_sched_group_barrier(0x100, R, 0);
+        if (i + A0 < N) __builtin_amdgcn_sched_group_barrier(0x100, R, 0);
     }
 }
 

@@ -22,6 +22,16 @@
 //   * Four waves (two pairs, 64 rows) per workgroup and two stages by
 //     default; eight waves (two per SIMD) and three stages are selectable at
 //     build time and measured no faster.
+//   * One wave per SIMD, so every stall is exposed: the operand reads of each
+//     MFMA chain are issued in fenced groups a fixed distance ahead (the
+//     compiler's own order left each MFMA waiting on its read), the second
+//     half of the probabilities is formed between the PV MFMAs that consume
+//     the first, and the row maximum crosses the two wave halves with a
+//     permlane swap.  The 128 output accumulators live in VGPRs (a per-file
+//     compiler option): left in AGPRs, every tile copied them out and back
+//     for the rarely taken rescale.
+//   * Rows wholly owned by one wave (all 576 score and 512 value channels, no
+//     exchange) would need 144 + 256 registers for Q^T and O and do not fit.
 #include <type_traits>
 
 #include "attn_common.h"
@@ -31,6 +41,9 @@
 #endif
 #ifndef PKV_MLA_WAVES
 #define PKV_MLA_WAVES 4
+#endif
+#ifndef PKV_MLA_AHEAD
+#define PKV_MLA_AHEAD 2   // LDS operand reads issued this many operands ahead of their MFMA
 #endif
 
 namespace pkv {
@@ -57,6 +70,7 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
     constexpr int PER = (NBLK + NW - 1) / NW;  // blocks of the busiest wave per tile
     constexpr int KS = DQK / 16 / 2;           // k-steps per wave (its half of the channels): 18
     constexpr int DB = DV / 64;                // 32-channel blocks per wave (its half of DV): 8
+    constexpr int RPW = NW / 2 * 32;           // rows per workgroup
     constexpr int TE = MBN * DQK;              // elements per tile
     static_assert(NW == 4 || NW == 8, "four or eight waves (pairs of waves share 32 rows)");
     static_assert(NS >= 2 && NS <= 4, "2..4 stages");
@@ -76,7 +90,7 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
     const SeqInfo si = seq_info(a, seq);
     const int H = a.n_heads;
     const int M = si.nq * H;
-    const int m0 = rb * (NW / 2 * 32);
+    const int m0 = rb * RPW;
     const int vhalf = (threadIdx.x >> 6) & 1;   // which 256-channel half of O this wave owns
     if (m0 >= M) return;
 
@@ -209,13 +223,23 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
         // Partial S^T = K Q^T over this wave's 288 channels, 32 keys (one
         // accumulation chain: dependent MFMAs on the same accumulator issue
         // back to back).
+        // Fenced groups: MFMA ks, then the read of the operand A steps ahead,
+        // so A LDS round trips stay in flight across the chain.
+        constexpr int A = PKV_MLA_AHEAD < KS ? PKV_MLA_AHEAD : KS;
+        auto k_operand = [&](int ks) __attribute__((always_inline)) {
+            return __builtin_bit_cast(bf16x8, *(const u32x4*)(ts + kofs[ks & 3] + (ks >> 2) * 64));
+        };
+        bf16x8 kop[KS];
+#pragma unroll
+        for (int ks = 0; ks < A; ++ks) kop[ks] = k_operand(ks);
+        __builtin_amdgcn_sched_barrier(0);
         f32x16 s = f32x16{};
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-            const u32x4 kv = *(const u32x4*)(ts + kofs[ks & 3] + (ks >> 2) * 64);
-            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kv), qf[ks], s, 0, 0, 0);
+            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[ks], qf[ks], s, 0, 0, 0);
+            if (ks + A < KS) kop[ks + A] = k_operand(ks + A);
+            __builtin_amdgcn_sched_barrier(0);
         }
-        sched_reads_mfma<KS, 1, 1>();
         // Exchange the partial scores with the other wave of the pair (the
         // lanes of both waves hold the same (key, row) elements).
         float* mine = xch + wave * 1024;
@@ -245,12 +269,16 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
             mx = -INFINITY;
 #pragma unroll
             for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[r]);
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            // lanes l and l + 32 hold the two 16-key halves of a row; a
+            // permlane swap pairs them without a trip through LDS
+            const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+            mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
         } else {
             mx = INFINITY;
 #pragma unroll
             for (int r = 0; r < 16; ++r) mx = fminf(mx, s[r]);
-            mx = fminf(mx, __shfl_xor(mx, 32));
+            const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+            mx = fminf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
         }
         const float msc = mx * sc2;
         const bool up = msc > m_run + kLazy;
@@ -264,8 +292,7 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
         }
         const float neg_m = m_run == -INFINITY ? 0.f : -m_run;
         float lsum = 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
+        auto prob = [&](int r) __attribute__((always_inline)) {
             float e = __builtin_amdgcn_exp2f(fmaf(s[r], sc2, neg_m));
             if (MASK) {
                 const int kk = t0 + (r >> 2) * 8 + hl * 4 + (r & 3);
@@ -273,34 +300,48 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
             }
             s[r] = e;
             lsum += e;
-        }
-        l_run += lsum;
-        bf16x8 pb[2];
-#pragma unroll
-        for (int st = 0; st < 2; ++st) {
+        };
+        auto pack = [&](int st) __attribute__((always_inline)) {
             f32x8 pv;
 #pragma unroll
             for (int e = 0; e < 8; ++e) pv[e] = s[st * 8 + e];
-            pb[st] = __builtin_convertvector(pv, bf16x8);
+            return __builtin_convertvector(pv, bf16x8);
+        };
+        // Probabilities of the first 16 keys now; those of the second 16 are
+        // formed between the MFMAs that consume the first (one per MFMA).
+        bf16x8 pb[2];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) prob(r);
+        pb[0] = pack(0);
+        // O^T += V^T P^T: V is channels 0..511 of the same tile; operand
+        // q = (16-key step q / DB, channel block q % DB), read A steps ahead.
+        constexpr int NQ = 2 * DB;
+        constexpr int AV = PKV_MLA_AHEAD < NQ ? PKV_MLA_AHEAD : NQ;
+        static_assert(DB == 8, "one second-half probability per first-half MFMA");
+        auto v_operand = [&](int q) __attribute__((always_inline)) {
+            const int st = q / DB, db = q % DB;
+            s16x4 part[2];
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+                part[b] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    PKV_LDS(s16x4, ts + vofs[db & 1][b] + st * 16 * DQK + (db >> 1) * 64));
+            const s16x4 p0 = part[0], p1 = part[1];
+            return __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){
+                                                  p0[0], p0[1], p0[2], p0[3], p1[0], p1[1], p1[2], p1[3]});
+        };
+        bf16x8 vop[NQ];
+#pragma unroll
+        for (int q = 0; q < AV; ++q) vop[q] = v_operand(q);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            o[q % DB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[q], pb[q / DB], o[q % DB], 0, 0, 0);
+            if (q < 8) prob(8 + q);
+            if (q == 7) pb[1] = pack(1);
+            if (q + AV < NQ) vop[q + AV] = v_operand(q + AV);
+            __builtin_amdgcn_sched_barrier(0);
         }
-        // O^T += V^T P^T: V is channels 0..511 of the same tile.
-#pragma unroll
-        for (int st = 0; st < 2; ++st) {
-#pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                s16x4 part[2];
-#pragma unroll
-                for (int b = 0; b < 2; ++b)
-                    part[b] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                        PKV_LDS(s16x4, ts + vofs[db & 1][b] + st * 16 * DQK + (db >> 1) * 64));
-                const s16x4 p0 = part[0], p1 = part[1];
-                const bf16x8 vf = __builtin_bit_cast(
-                    bf16x8, (short __attribute__((ext_vector_type(8)))){p0[0], p0[1], p0[2], p0[3], p1[0], p1[1],
-                                                                          p1[2], p1[3]});
-                o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[st], o[db], 0, 0, 0);
-            }
-        }
-        sched_reads_mfma<2 * DB, 2, 1>();
+        l_run += lsum;
     };
 
     // Each wave waits for its own loads: n_mine per tile (PER or PER - 1).
