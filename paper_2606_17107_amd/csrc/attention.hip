@@ -7,6 +7,9 @@
 #ifndef PKV_ATTN_SHAPE
 #define PKV_ATTN_SHAPE 1       // bf16 GQA kernel: 0 plain order (64-key tiles), 1 pipelined (32-key tiles)
 #endif
+#ifndef PKV_ATTN_QB
+#define PKV_ATTN_QB 1          // bf16 GQA pipelined kernel: 32-row blocks per wave
+#endif
 #ifndef PKV_MLA_STAGES
 #define PKV_MLA_STAGES 2       // LDS pipeline depth of the MLA kernel
 #endif
@@ -172,7 +175,7 @@ Plan make_plan(const AttnArgs& a, int splits) {
     } else {
         // bf16 GQA: 4 waves x 32 rows, two workgroups per CU; pipelined over
         // 32-key tiles in 4 LDS stages, or plain order over 64-key tiles in 2.
-        p.qb = 1;
+        p.qb = PKV_ATTN_SHAPE == 1 ? PKV_ATTN_QB : 1;
         p.nw = 4;
         p.ns = PKV_ATTN_SHAPE == 1 ? 4 : 2;
         tile = PKV_ATTN_SHAPE == 1 ? 32 : 64;
@@ -191,6 +194,7 @@ Plan make_plan(const AttnArgs& a, int splits) {
 // Workgroups that fit on one CU at once (LDS and register bound).
 int wgs_per_cu(const AttnArgs& a, const Plan& p) {
     if (a.variant == 1) return 1;                     // MLA: 36 KB stages plus the score exchange
+    if (p.qb > 1) return 1;                           // 64 rows per wave: one wave per SIMD (registers)
     const int tile = p.ns == 4 ? 32 : 64;             // keys per K/V tile
     const int lds = p.ns * 2 * tile * a.head_dim * 2;
     const int n = (160 * 1024) / lds;

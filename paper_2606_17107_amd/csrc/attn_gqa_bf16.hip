@@ -26,6 +26,9 @@ namespace pkv {
 namespace {
 
 
+#ifndef PKV_ATTN_QB
+#define PKV_ATTN_QB 1      // 32-row blocks per wave of the pipelined kernel
+#endif
 #ifndef PKV_ATTN_AHEAD
 #define PKV_ATTN_AHEAD 3   // LDS operand reads issued this many operands ahead of their MFMA
 #endif
@@ -57,7 +60,7 @@ __device__ inline int swz_v(int key) {
 }
 
 template <int D, int QB, int NW, int NS, bool PIPE, bool PAGED>
-__global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, Plan p) {
+__global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel(AttnArgs a, Plan p) {
     constexpr int CH = D / 8;              // 16-byte chunks per row
     constexpr int BN = PIPE ? 32 : 64;     // keys per tile
     constexpr int NKB = BN / 32;           // 32-key blocks per tile
@@ -707,9 +710,10 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, P
 //   ns == 2: 64-key tiles, plain order (64 KB of LDS stages).
 template <int D, bool PAGED>
 hipError_t launch_d(const AttnArgs& a, const Plan& p, dim3 grid, hipStream_t stream) {
-    if (p.nw != 4 || p.qb != 1) return hipErrorInvalidValue;
+    if (p.nw != 4 || p.qb != PKV_ATTN_QB) return hipErrorInvalidValue;
     if (p.ns == 4)
-        hipLaunchKernelGGL((attn_gqa_bf16_kernel<D, 1, 4, 4, true, PAGED>), grid, dim3(256), 0, stream, a, p);
+        hipLaunchKernelGGL((attn_gqa_bf16_kernel<D, PKV_ATTN_QB, 4, 4, true, PAGED>), grid, dim3(256), 0, stream, a,
+                           p);
     else if (p.ns == 2 && (!PAGED || a.page_shift >= 6))   // 64-key tiles need pages of 64 slots or more
         hipLaunchKernelGGL((attn_gqa_bf16_kernel<D, 1, 4, 2, false, PAGED>), grid, dim3(256), 0, stream, a, p);
     else
