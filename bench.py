@@ -415,10 +415,13 @@ def source_hash(files):
     return h.hexdigest()[:16]
 
 
-KERNEL_SOURCES = {
-    "splice_kernel": ["paper_2606_17107_amd/csrc/splice.hip"],
-    "attn_gqa_bf16": ["paper_2606_17107_amd/csrc/attn_gqa_bf16.hip", "paper_2606_17107_amd/csrc/attn_common.h"],
-    "attn_mla_bf16": ["paper_2606_17107_amd/csrc/attn_mla_bf16.hip", "paper_2606_17107_amd/csrc/attn_common.h"],
+KERNEL_SOURCES = {   # the sources and compiler options each kernel is built from
+    "splice_kernel": ["paper_2606_17107_amd/csrc/splice.hip", "paper_2606_17107_amd/csrc/pkv_internal.h",
+                      "paper_2606_17107_amd/build.py"],
+    "attn_gqa_bf16": ["paper_2606_17107_amd/csrc/attn_gqa_bf16.hip", "paper_2606_17107_amd/csrc/attn_common.h",
+                      "paper_2606_17107_amd/csrc/pkv_internal.h", "paper_2606_17107_amd/build.py"],
+    "attn_mla_bf16": ["paper_2606_17107_amd/csrc/attn_mla_bf16.hip", "paper_2606_17107_amd/csrc/attn_common.h",
+                      "paper_2606_17107_amd/csrc/pkv_internal.h", "paper_2606_17107_amd/build.py"],
 }
 
 
