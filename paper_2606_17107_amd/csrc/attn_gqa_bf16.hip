@@ -26,6 +26,12 @@ namespace pkv {
 namespace {
 
 
+#ifndef PKV_ATTN_PRIO
+#define PKV_ATTN_PRIO 2    // wave priority raised over bit 0: the score segment, bit 1: the PV segment
+#endif
+#ifndef PKV_ATTN_PRIO_LEVEL
+#define PKV_ATTN_PRIO_LEVEL 1
+#endif
 #ifndef PKV_ATTN_QB
 #define PKV_ATTN_QB 1      // 32-row blocks per wave of the pipelined kernel
 #endif
@@ -440,7 +446,10 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
         // workgroups of four waves share each CU, so the two waves on a SIMD
         // never wait at each other's barriers.  Iteration t reads K of tile
         // t+1 and V of tile t; tile t+3 is issued after the barrier opening
-        // it, into the stage that tile t-1 left.
+        // it, into the stage that tile t-1 left.  A wave raises its priority
+        // for segment 2, so of the two waves on a SIMD the one streaming the
+        // PV MFMAs issues first and the other fills in with segment 1's VALU
+        // work (measured 5% on the 8B workload, 1% on the 32k one).
         static_assert(NS >= 4 && NS % 2 == 0 && NKB == 1,
                       "the pipelined schedule uses an even number (>= 4) of LDS stages of 32-key tiles");
         // (With a sliding window every tile goes through the masked plain order.)
@@ -561,8 +570,19 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
                              f32x16 (&nxt)[QB]) __attribute__((always_inline)) {
             bf16x8 pb[QB][2];
             float mx[QB];
+#if PKV_ATTN_PRIO & 1
+            __builtin_amdgcn_s_setprio(1);
+#endif
             seg1(ks_next, kbn, cur, nxt, pb);
+#if PKV_ATTN_PRIO & 2
+            __builtin_amdgcn_s_setprio(PKV_ATTN_PRIO_LEVEL);
+#elif PKV_ATTN_PRIO & 1
+            __builtin_amdgcn_s_setprio(0);
+#endif
             seg2(vs_cur, kbc, pb, nxt, mx);
+#if PKV_ATTN_PRIO & 2
+            __builtin_amdgcn_s_setprio(0);
+#endif
             move_max(mx);
         };
 
