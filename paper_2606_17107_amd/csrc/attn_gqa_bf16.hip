@@ -83,7 +83,7 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
     // operand serves every stage through the 16-bit immediate offset of the
     // LDS read (K stages within 48 KB of the block, V stages of the V half).
     __shared__ __attribute__((aligned(16))) uint16_t stage_lds[2 * NS * TE];
-    __shared__ int red[NW], red_min[NW], red_start[NW];
+    __shared__ int red[NW], red_min[NW], red_start[NW], red_smax[NW];
     auto kst = [&](int st) -> uint16_t* __attribute__((always_inline)) { return stage_lds + st * TE; };
     auto vst = [&](int st) -> uint16_t* __attribute__((always_inline)) { return stage_lds + (NS + st) * TE; };
 
@@ -136,14 +136,16 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
         red[wave] = wmax;
         red_min[wave] = wmin;
         red_start[wave] = wsmin;
+        red_smax[wave] = wsmax;
     }
     __syncthreads();
-    int e_max = 0, e_min = 0x7fffffff, s_min = 0x7fffffff;
+    int e_max = 0, e_min = 0x7fffffff, s_min = 0x7fffffff, s_max = 0;
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
         e_max = max(e_max, red[w]);
         e_min = min(e_min, red_min[w]);
         s_min = min(s_min, red_start[w]);
+        s_max = max(s_max, red_smax[w]);
     }
 
     // Tiles wholly before every row's window start are skipped.
@@ -379,6 +381,19 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
         sched_reads_mfma<2 * NKB * DB, 2, QB>();
     };
 
+    // Processing order.  The pipelined schedule takes the F tiles that need
+    // no mask for any row of the workgroup (key range [s_max, e_min): past
+    // every row's window start, before every row's end) first; the n_lead
+    // tiles before s_max and the tail after them follow in plain order with
+    // masks.  Online softmax does not depend on the order of the tiles.
+    // Without a window n_lead is 0 and the order is ascending.
+    const int n_lead = PIPE && a.window > 0 ? min(n_tiles, max(0, (s_max - k_begin + BN - 1) / BN)) : 0;
+    const int F = PIPE && sc2 > 0.f ? max(0, min(n_tiles - n_lead, (e_min - (k_begin + n_lead * BN)) / BN)) : 0;
+    auto key_of = [&](int i) __attribute__((always_inline)) {
+        const int t = i < F ? i + n_lead : (i < F + n_lead ? i - F : i);
+        return k_begin + t * BN;
+    };
+
     // Tiles are staged through NS LDS stages: tile i lives in stage i % NS
     // and is issued NS-1 tiles ahead of its use.  Wait until at most
     // tiles_after later tiles (at most NS-2) are still in flight.
@@ -403,11 +418,11 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
         lds_reads_done();
         bare_barrier();
         const int ahead = i + NS - 1;
-        if (ahead < n_tiles) issue(k_begin + ahead * BN, kst((S + NS - 1) % NS), vst((S + NS - 1) % NS));
+        if (ahead < n_tiles) issue(key_of(ahead), kst((S + NS - 1) % NS), vst((S + NS - 1) % NS));
         f32x16 sc[NKB][QB];
         qk(kst(S), sc);
         bf16x8 pb[QB][2 * NKB];
-        const int t0 = k_begin + i * BN;
+        const int t0 = key_of(i);
         if (t0 + BN > wmin || t0 < wsmax) {
             row_max(t0, sc, std::true_type{});
             probs(t0, sc, pb, std::true_type{});
@@ -428,7 +443,7 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
 
 #pragma unroll
     for (int s = 0; s < NS - 1; ++s)
-        if (s < n_tiles) issue(k_begin + s * BN, kst(s), vst(s));
+        if (s < n_tiles) issue(key_of(s), kst(s), vst(s));
 
     if constexpr (!PIPE) {
         plain_from(0);
@@ -452,8 +467,7 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
         // work (measured 5% on the 8B workload, 1% on the 32k one).
         static_assert(NS >= 4 && NS % 2 == 0 && NKB == 1,
                       "the pipelined schedule uses an even number (>= 4) of LDS stages of 32-key tiles");
-        // (With a sliding window every tile goes through the masked plain order.)
-        const int F = sc2 > 0.f && a.window == 0 ? max(0, min(n_tiles, (e_min - k_begin) / BN)) : 0;
+
         const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
         // Segment 1: nxt = raw scores of key block kbn of the K stage; the
@@ -592,7 +606,7 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
             lds_reads_done();
             bare_barrier();
             if (i + NS - 1 < n_tiles)
-                issue(k_begin + (i + NS - 1) * BN, kst((U + NS - 1) % NS), vst((U + NS - 1) % NS));
+                issue(key_of(i + NS - 1), kst((U + NS - 1) % NS), vst((U + NS - 1) % NS));
             half_step(kst((U + 1) % NS), 0, vst(U), 0, cur, nxt);
         };
 
@@ -603,7 +617,7 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
             lds_reads_done();
             bare_barrier();
             if (i + NS - 1 < n_tiles)
-                issue(k_begin + (i + NS - 1) * BN, kst((U + NS - 1) % NS), vst((U + NS - 1) % NS));
+                issue(key_of(i + NS - 1), kst((U + NS - 1) % NS), vst((U + NS - 1) % NS));
             bf16x8 pb[QB][2];
 #pragma unroll
             for (int qb = 0; qb < QB; ++qb) {
