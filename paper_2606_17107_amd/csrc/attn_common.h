@@ -159,7 +159,7 @@ __device__ inline uint64_t uniform_u64(uint64_t v) {
 #ifndef PKV_LDS_DMA16
 __device__ inline void lds_dma_asm(uint32_t m0, uint64_t sbase, uint32_t voff) {
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(m0), "v"(voff), "s"(sbase)
-                 : "memory");
+                 : "memory", "m0");
 }
 
 // LDS byte address of a pointer into a __shared__ array (the low 32 bits of
