@@ -1,0 +1,130 @@
+"""GPU edge cases against the oracle: deltas at the limit the ABI states
+(|delta| < 2^24) on the uniform and the per-lane coefficient paths, GQA group
+sizes 1 (MHA) and 8, calls with nothing to do, and a sequence with no cache
+slots.  Bars as in the other parity tests."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from helpers import bits_to_f64, check_attention_close, check_rotated_keys, dev, host_bits, log
+from paper_2606_17107_amd import pkv, synth
+
+pytestmark = pytest.mark.gpu
+
+LIMIT = (1 << 24) - 1
+
+
+def bits(shape, seed):
+    return host_bits(synth.Draws(seed, "cpu").normal(shape))
+
+
+def splice_case(deltas, d=128, v_dim=128, r=128, offset=0, style=0, theta=5e5, seed=0):
+    n = len(deltas)
+    L, H = 2, 2
+    sk = bits((L, H, n, d), seed)
+    sv = bits((L, H, n, v_dim), seed + 1) if v_dim else None
+    dk = bits((L, H, n, d), seed + 2)
+    dv = bits((L, H, n, v_dim), seed + 3) if v_dim else None
+    dst = np.arange(n, dtype=np.int64)
+    src = dst - np.asarray(deltas, np.int64)
+    assert src.min() >= -(1 << 31) and src.max() < (1 << 31)
+    src, dst = src.astype(np.int32), dst.astype(np.int32)
+    gk, gv = dev(dk), (dev(dv) if v_dim else None)
+    pkv.reposition_splice(dev(sk), dev(sv) if v_dim else None, gk, gv, torch.from_numpy(src).cuda(),
+                          torch.from_numpy(dst).cuda(), theta, r, offset, style)
+    torch.cuda.synchronize()
+    ok, ov = dk.copy(), (dv.copy() if v_dim else None)
+    oracle.reposition_splice(sk, sv, ok, ov, src, dst, theta, r, offset, style)
+    if v_dim:
+        np.testing.assert_array_equal(host_bits(gv), ov)
+    return check_rotated_keys(host_bits(gk), ok, offset, r, style)
+
+
+def test_uniform_delta_at_the_limit():
+    """Every token moves by 2^24 - 1 (the wave-uniform coefficient path), and by -(2^24 - 1)."""
+    for sign in (1, -1):
+        n_diff, n_floor = splice_case([sign * LIMIT] * 96, seed=10)
+        log("  delta %+d: K not bit-equal %d, floor %d" % (sign * LIMIT, n_diff, n_floor))
+
+
+def test_mixed_large_deltas():
+    """Per-token deltas spread over (-2^24, 2^24) (the per-lane path), GQA rows and MLA k_pe."""
+    rng = np.random.default_rng(11)
+    deltas = np.concatenate([[LIMIT, -LIMIT, 1 << 23, -(1 << 23), 1, -1, 0],
+                             rng.integers(-LIMIT, LIMIT + 1, 121)])
+    splice_case(deltas, seed=12)
+    splice_case(deltas, d=576, v_dim=0, r=64, offset=512, style=1, theta=1e4, seed=13)
+
+
+@pytest.mark.parametrize("H,Hkv,d", [(4, 4, 128), (16, 2, 128), (8, 8, 64), (16, 2, 64)])
+def test_group_sizes(H, Hkv, d):
+    """GQA groups of 1 (multi-head attention) and 8 query heads per KV head."""
+    L, n_q, kv = 2, 37, 611
+    g = synth.Draws(20 + H + d, "cpu")
+    q = host_bits(g.normal((L, n_q, H, d)))
+    k = host_bits(g.normal((L, Hkv, kv, d)))
+    v = host_bits(g.normal((L, Hkv, kv, d)))
+    q_pos = np.arange(kv - n_q, kv, dtype=np.int32)
+    scale = 1 / np.sqrt(d)
+    for splits in (1, 3):
+        out = torch.zeros(L, n_q, H, d, dtype=torch.bfloat16, device="cuda")
+        pkv.suffix_attention(dev(q), dev(k), dev(v), out, torch.from_numpy(q_pos).cuda(),
+                             torch.tensor([kv], dtype=torch.int32, device="cuda"), scale, max_kv_len=kv,
+                             n_splits=splits)
+        torch.cuda.synchronize()
+        got = host_bits(out)
+        for l in range(L):
+            want, _ = oracle.attention(q[l], k[l], v[l], q_pos, kv, scale)
+            check_attention_close(got[l], want)
+
+
+def test_calls_with_nothing_to_do():
+    """n_tokens = 0 splices nothing; total_q = 0 attends nothing; both return OK and touch nothing."""
+    g = synth.Draws(30, "cuda")
+    sk, sv = g.normal((1, 2, 4, 128)), g.normal((1, 2, 4, 128))
+    dk, dv = g.normal((1, 2, 16, 128)), g.normal((1, 2, 16, 128))
+    before = (dk.clone(), dv.clone())
+    pos = torch.zeros(4, dtype=torch.int32, device="cuda")
+    layout = pkv.make_layout(sk, sv, dk, dv, n_tokens=0)
+    assert pkv.pkv_reposition_splice(sk, sv, dk, dv, pos, pos, 1e4, 128, layout) == pkv.PKV_OK
+    q = g.normal((1, 3, 4, 128))
+    out = torch.full((1, 3, 4, 128), 5.0, dtype=torch.bfloat16, device="cuda")
+    desc = pkv.make_attn_desc(q, dk, dv, out, 16)
+    desc.total_q = desc.max_q = 0
+    kl = torch.tensor([16], dtype=torch.int32, device="cuda")
+    assert pkv.pkv_suffix_attention(q, dk, dv, out, pos, kl, 4, 2, 128, 0.1, desc, None, 0) == pkv.PKV_OK
+    torch.cuda.synchronize()
+    assert torch.equal(dk, before[0]) and torch.equal(dv, before[1])
+    assert bool((out == 5.0).all())
+
+
+def test_sequence_without_slots():
+    """In a ragged call a sequence with kv_len 0 gets zero rows and LSE -inf; its neighbours are exact."""
+    H, Hkv, d, L = 8, 2, 128, 1
+    nqs, kvls = [5, 9, 7], [300, 0, 450]
+    caps = [max(kl, 1) + 3 for kl in kvls]
+    bases = np.concatenate([[0], np.cumsum(caps)[:-1]]).astype(np.int64)
+    g = synth.Draws(31, "cpu")
+    k = host_bits(g.normal((L, Hkv, int(sum(caps)), d)))
+    v = host_bits(g.normal((L, Hkv, int(sum(caps)), d)))
+    q = host_bits(g.normal((L, sum(nqs), H, d)))
+    q_pos = np.concatenate([np.arange(max(kl - n, 0), max(kl - n, 0) + n) for n, kl in zip(nqs, kvls)]).astype(
+        np.int32)
+    cu = np.concatenate([[0], np.cumsum(nqs)]).astype(np.int32)
+    out = torch.full((L, sum(nqs), H, d), 7.0, dtype=torch.bfloat16, device="cuda")
+    lse = torch.zeros(L, sum(nqs), H, dtype=torch.float32, device="cuda")
+    pkv.suffix_attention(dev(q), dev(k), dev(v), out, torch.from_numpy(q_pos).cuda(),
+                         torch.tensor(kvls, dtype=torch.int32, device="cuda"), 1 / np.sqrt(d), max_kv_len=max(kvls),
+                         n_seqs=3, cu_q=torch.from_numpy(cu).cuda(), kv_base=torch.from_numpy(bases).cuda(),
+                         max_q=max(nqs), lse_out=lse)
+    torch.cuda.synchronize()
+    got, lse = host_bits(out), lse.cpu().numpy()
+    empty = slice(cu[1], cu[2])
+    assert np.all(bits_to_f64(got[:, empty]) == 0) and np.all(np.isneginf(lse[:, empty]))
+    for s in (0, 2):
+        rows = slice(cu[s], cu[s + 1])
+        ks = slice(bases[s], bases[s] + caps[s])
+        want, _ = oracle.attention(np.ascontiguousarray(q[0, rows]), np.ascontiguousarray(k[0][:, ks]),
+                                   np.ascontiguousarray(v[0][:, ks]), q_pos[rows], kvls[s], 1 / np.sqrt(d))
+        check_attention_close(got[0, rows], want)
