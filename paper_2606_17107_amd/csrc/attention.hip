@@ -211,20 +211,26 @@ int attention_splits(const AttnArgs& a) {
         if (s > max_s) s = max_s < 1 ? 1 : max_s;
         return s;
     }
-    // Pick the split count that minimises the estimated time: workgroup rounds
-    // over the CUs divided by the split factor (each split does 1/s of the
-    // keys), with a 10% charge for the combine pass and its workspace; at least 256 keys per
-    // split.
+    // Pick the split count that minimises the estimated time: the workgroup
+    // rounds over the CUs times the duration of one workgroup (1/s of the
+    // keys), plus, for s > 1, the split partials written and read back by the
+    // combine pass.  Nominal rates (measured on MI355X): the bf16 kernels
+    // sustain about 1.0 PFLOP/s (GQA) and 0.75 PFLOP/s (MLA), the combine
+    // streams at about 5 TB/s.  At least 256 keys per split.
     const Plan p = make_plan(a, 1);
     const int64_t wgs = (int64_t)p.n_groups * p.rbs;
     const int64_t slots = 256 * (int64_t)wgs_per_cu(a, p);
+    const double rate = a.variant == 1 ? 0.75e15 : 1.0e15;
+    const double wg_flops = (double)p.BM * a.max_kv_len * (a.head_dim + a.head_dim_v) * 2.0;
+    const double slot_rate = rate / (double)slots;
+    const double comb_bytes = (double)a.n_layers * a.total_q * a.n_heads * (a.head_dim_v + 1) * 4.0 * 2.0;
     int best = 1;
     double best_t = 1e30;
     for (int s = 1; s <= 8; ++s) {
         if (s > 1 && a.max_kv_len / s < 256) break;
         const double rounds = (double)((wgs * s + slots - 1) / slots);
-        const double t = rounds / s * (s > 1 ? 1.10 : 1.0);
-        if (t < best_t - 1e-9) {
+        const double t = rounds * (wg_flops / s) / slot_rate + (s > 1 ? s * comb_bytes / 5e12 + 5e-6 : 0.0);
+        if (t < best_t * (1.0 - 1e-9)) {
             best_t = t;
             best = s;
         }
