@@ -419,9 +419,11 @@ KERNEL_SOURCES = {   # the sources and compiler options each kernel is built fro
     "splice_kernel": ["paper_2606_17107_amd/csrc/splice.hip", "paper_2606_17107_amd/csrc/pkv_internal.h",
                       "paper_2606_17107_amd/build.py"],
     "attn_gqa_bf16": ["paper_2606_17107_amd/csrc/attn_gqa_bf16.hip", "paper_2606_17107_amd/csrc/attn_common.h",
-                      "paper_2606_17107_amd/csrc/pkv_internal.h", "paper_2606_17107_amd/build.py"],
+                      "paper_2606_17107_amd/csrc/attention.hip", "paper_2606_17107_amd/csrc/pkv_internal.h",
+                      "paper_2606_17107_amd/build.py"],
     "attn_mla_bf16": ["paper_2606_17107_amd/csrc/attn_mla_bf16.hip", "paper_2606_17107_amd/csrc/attn_common.h",
-                      "paper_2606_17107_amd/csrc/pkv_internal.h", "paper_2606_17107_amd/build.py"],
+                      "paper_2606_17107_amd/csrc/attention.hip", "paper_2606_17107_amd/csrc/pkv_internal.h",
+                      "paper_2606_17107_amd/build.py"],
 }
 
 
