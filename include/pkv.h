@@ -158,7 +158,9 @@ pkv_status pkv_reposition_splice_freqs(const void* src_k, const void* src_v, voi
  * o*stride[2] + c, with stride[] the {layer, head, slot} element strides of
  * the layout / descriptor passed alongside (V likewise with page_stride_v).
  * A pool laid out [layer][page][slot][kv_head][d] has stride = {n_pages *
- * page_size * Hkv * d, d, Hkv * d} and page_stride = page_size * Hkv * d. */
+ * page_size * Hkv * d, d, Hkv * d} and page_stride = page_size * Hkv * d.
+ * With v_block_table set, V slot p is in page v_block_table[s * max_pages +
+ * p / page_size] instead (same page size, pool size and clamping rules). */
 typedef struct pkv_paged_cache {
     int32_t page_size;           /* slots per page: a power of two, 32 .. 2^20 */
     int32_t max_pages;           /* block_table entries per sequence */
@@ -166,14 +168,19 @@ typedef struct pkv_paged_cache {
     int64_t n_pages;             /* physical pages in the pool */
     int64_t page_stride_k;       /* elements between consecutive physical pages of K */
     int64_t page_stride_v;       /* ... of V (unused when there is no V tensor) */
+    const int32_t* v_block_table;  /* optional device int32 [n_seqs][max_pages]: V pages through
+                                      their own table (NULL: block_table for both).  Values are
+                                      position-free, so a spliced chunk's value pages can be
+                                      referenced in place instead of copied (GQA only). */
 } pkv_paged_cache;
 
 /* Reposition + splice into a paged destination cache: as pkv_reposition_splice
  * with the destination slot dst_pos[t] taken as a logical slot of the sequence
  * whose block table is row 0 of paging->block_table.  layout->dst_capacity is
  * the logical capacity (at most max_pages * page_size) and the dst strides are
- * {layer, head, in-page slot}.  A token whose slot or page entry is out of
- * range is skipped (and *err_flag set).  The source is a contiguous chunk as
+ * {layer, head, in-page slot}; values go through paging->v_block_table when it
+ * is set.  A token whose slot or page entry is out of range is skipped (and
+ * *err_flag set).  The source is a contiguous chunk as
  * in pkv_reposition_splice.
  * Errors: as pkv_reposition_splice; PKV_ERR_NULL (paging or its block table),
  * PKV_ERR_SHAPE (page_size not a power of two in [32, 2^20], non-positive
@@ -291,8 +298,8 @@ pkv_status pkv_suffix_attention(const void* q, const void* k_cache, const void* 
  * clamped so that every read stays inside the pool (the slots they map are then
  * undefined).  bf16 only (GQA and MLA).
  * Errors: as pkv_suffix_attention; PKV_ERR_NULL (paging, block table),
- * PKV_ERR_SHAPE (paging fields as for the paged splice, kv_base given),
- * PKV_ERR_UNSUPPORTED (fp32). */
+ * PKV_ERR_SHAPE (paging fields as for the paged splice, kv_base given,
+ * v_block_table with MLA), PKV_ERR_UNSUPPORTED (fp32). */
 pkv_status pkv_suffix_attention_paged(const void* q, const void* k_pages, const void* v_pages, void* out,
                                       const int32_t* q_pos, const int32_t* kv_len, int32_t n_q_heads,
                                       int32_t n_kv_heads, int32_t head_dim, float scale,

@@ -191,6 +191,7 @@ pkv_status check_splice(const void* src_k, const void* src_v, void* dst_k, void*
     a.err_flag = L->err_flag;
     if (pg) {
         a.dst_pages = pg->block_table;
+        a.dst_v_pages = pg->v_block_table;
         a.page_shift = page_shift;
         a.max_pages = pg->max_pages;
         a.n_pages = pg->n_pages;
@@ -248,9 +249,9 @@ pkv_status check_attention(const void* q, const void* k, const void* v, void* ou
         if (d->kv_base) return fail(PKV_ERR_SHAPE, "desc.kv_base must be NULL for a paged cache");
         pkv_status st = check_paging(pg, d->cache_slots, eb, &page_shift);
         if (st != PKV_OK) return st;
-        if (d->variant == PKV_ATTN_MLA && pg->page_stride_v != pg->page_stride_k)
+        if (d->variant == PKV_ATTN_MLA && (pg->page_stride_v != pg->page_stride_k || pg->v_block_table))
             return fail(PKV_ERR_SHAPE, "MLA reads values from the latent channels: page_stride_v must equal "
-                                       "page_stride_k");
+                                       "page_stride_k and there is no separate v_block_table");
     }
     // out must not overlap any input
     if (check_alias && d->total_q > 0) {
@@ -302,6 +303,7 @@ pkv_status check_attention(const void* q, const void* k, const void* v, void* ou
     }
     if (pg) {
         a.block_table = pg->block_table;
+        a.v_block_table = pg->v_block_table;
         a.page_shift = page_shift;
         a.max_pages = pg->max_pages;
         a.n_pages = pg->n_pages;

@@ -82,7 +82,7 @@ __device__ inline SeqInfo seq_info(const AttnArgs& a, int seq) {
 // order, so the window moves forward a whole window at a time; each entry is
 // clamped into the pool when loaded, so every tile read stays inside it.
 struct PageWindow {
-    const int32_t* row;   // block_table + seq * max_pages
+    const int32_t* row;   // the sequence's row of the block table
     int n_entries;        // max_pages
     int last_page;        // n_pages - 1
     int w0;               // first entry in the window
@@ -100,8 +100,8 @@ struct PageWindow {
         id2 = entry(l + 128);
         id3 = entry(l + 192);
     }
-    __device__ __forceinline__ void init(const AttnArgs& a, int seq, int first_entry) {
-        row = a.block_table + (int64_t)seq * a.max_pages;
+    __device__ __forceinline__ void init(const int32_t* table, const AttnArgs& a, int seq, int first_entry) {
+        row = table + (int64_t)seq * a.max_pages;
         n_entries = a.max_pages;
         last_page = (int)(a.n_pages - 1);
         load(first_entry);

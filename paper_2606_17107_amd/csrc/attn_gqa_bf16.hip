@@ -197,7 +197,9 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
     // Paged cache: tiles start on a multiple of BN, which divides the page
     // size, so each tile lies in one page.
     PageWindow pw;
-    if constexpr (PAGED) pw.init(a, seq, k_begin >> a.page_shift);
+    // Waves that move V blocks read V's own block table when there is one.
+    if constexpr (PAGED)
+        pw.init(wave_v && a.v_block_table ? a.v_block_table : a.block_table, a, seq, k_begin >> a.page_shift);
     const int64_t tpage = (wave_v ? a.v_page_stride : a.k_page_stride) * 2;   // bytes between pages
     auto issue = [&](int t0, uint16_t* ks_dst, uint16_t* vs_dst) __attribute__((always_inline)) {
         const char* tile;

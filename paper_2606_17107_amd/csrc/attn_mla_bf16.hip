@@ -161,7 +161,7 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
     }
     // Paged cache: a 32-key tile lies in one page (page sizes are multiples of 32).
     PageWindow pw;
-    if constexpr (PAGED) pw.init(a, seq, k_begin >> a.page_shift);
+    if constexpr (PAGED) pw.init(a.block_table, a, seq, k_begin >> a.page_shift);
     auto issue = [&](int t0, uint16_t* dst_stage) {
         const char* kt;
         if constexpr (PAGED)

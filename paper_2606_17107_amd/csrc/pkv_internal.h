@@ -52,6 +52,7 @@ struct SpliceArgs {
     // paged destination (per-token mode): logical slot p -> page
     // dst_pages[p >> page_shift], in-page slot p & (page_size - 1)
     const int32_t* dst_pages;  // null: contiguous destination
+    const int32_t* dst_v_pages;  // V through its own table, or null (dst_pages)
     int32_t page_shift;
     int32_t max_pages;
     int64_t n_pages;
@@ -97,6 +98,7 @@ struct AttnArgs {
     // paged cache: sequence s's slot p is in page block_table[s * max_pages +
     // (p >> page_shift)], in-page slot p & (page_size - 1)
     const int32_t* block_table;  // null: contiguous cache
+    const int32_t* v_block_table;  // V through its own table, or null (block_table)
     int32_t page_shift;
     int32_t max_pages;
     int64_t n_pages;

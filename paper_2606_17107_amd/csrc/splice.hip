@@ -365,7 +365,8 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
         bool page_ok = true;
         if constexpr (PAGED) {
             const int64_t pidx = work ? dst_slot >> a.page_shift : 0;
-            const int32_t page = a.dst_pages[pidx];
+            const int32_t* table = !is_k && a.dst_v_pages ? a.dst_v_pages : a.dst_pages;
+            const int32_t page = table[pidx];
             page_ok = page >= 0 && page < a.n_pages;
             dst_row = (int64_t)page * dpg + (dst_slot & ((1 << a.page_shift) - 1)) * d2;
         } else {

@@ -69,6 +69,7 @@ class pkv_paged_cache(ctypes.Structure):
     _fields_ = [
         ("page_size", ctypes.c_int32), ("max_pages", ctypes.c_int32), ("block_table", ctypes.c_void_p),
         ("n_pages", ctypes.c_int64), ("page_stride_k", ctypes.c_int64), ("page_stride_v", ctypes.c_int64),
+        ("v_block_table", ctypes.c_void_p),
     ]
 
 
@@ -351,9 +352,12 @@ def pool_strides3(pool: Optional[torch.Tensor]):
     return _i64x3(pool.stride(0), pool.stride(3), pool.stride(2))
 
 
-def make_paging(block_table: torch.Tensor, k_pool: torch.Tensor,
-                v_pool: Optional[torch.Tensor] = None) -> pkv_paged_cache:
+def make_paging(block_table: torch.Tensor, k_pool: torch.Tensor, v_pool: Optional[torch.Tensor] = None,
+                v_block_table: Optional[torch.Tensor] = None) -> pkv_paged_cache:
     assert block_table.dtype == torch.int32 and block_table.dim() == 2 and block_table.is_contiguous()
+    if v_block_table is not None:
+        assert v_block_table.dtype == torch.int32 and v_block_table.shape == block_table.shape
+        assert v_block_table.is_contiguous()
     pg = pkv_paged_cache()
     pg.page_size = k_pool.shape[2]
     pg.max_pages = block_table.shape[1]
@@ -361,26 +365,27 @@ def make_paging(block_table: torch.Tensor, k_pool: torch.Tensor,
     pg.n_pages = k_pool.shape[1]
     pg.page_stride_k = k_pool.stride(1)
     pg.page_stride_v = 0 if v_pool is None else v_pool.stride(1)
+    pg.v_block_table = None if v_block_table is None else v_block_table.data_ptr()
     return pg
 
 
 def reposition_splice_paged(src_k, src_v, k_pool, v_pool, src_pos, dst_pos, block_table, rope_theta, rope_dim,
                             rope_offset=0, rope_style=PKV_ROPE_HALF, dst_capacity=None, err_flag=None,
-                            stream=None) -> None:
+                            stream=None, v_block_table=None) -> None:
     """Tensor-level call of pkv_reposition_splice_paged: destination slots are logical slots of the
     sequence whose block-table row is block_table[0]."""
     L = make_layout(src_k, src_v, src_k, src_v, rope_offset, rope_style, err_flag=err_flag)
     L.dst_capacity = (block_table.shape[1] * k_pool.shape[2]) if dst_capacity is None else int(dst_capacity)
     L.dst_k_stride = pool_strides3(k_pool)
     L.dst_v_stride = pool_strides3(v_pool)
-    pg = make_paging(block_table, k_pool, v_pool)
+    pg = make_paging(block_table, k_pool, v_pool, v_block_table)
     _check(pkv_reposition_splice_paged(src_k, src_v, k_pool, v_pool, src_pos, dst_pos, rope_theta, rope_dim, L, pg,
                                        stream))
 
 
 def suffix_attention_paged(q, k_pool, v_pool, out, q_pos, kv_len, block_table, scale, max_kv_len, n_seqs=1,
                            cu_q=None, max_q=None, variant=PKV_ATTN_GQA, n_splits=0, lse_out=None, workspace=None,
-                           stream=None, window=0, cache_slots=None) -> None:
+                           stream=None, window=0, cache_slots=None, v_block_table=None) -> None:
     """Tensor-level call of pkv_suffix_attention_paged (q [L][rows][H][d], pools as above)."""
     H = q.shape[2]
     Hkv = k_pool.shape[3]
@@ -405,7 +410,7 @@ def suffix_attention_paged(q, k_pool, v_pool, out, q_pos, kv_len, block_table, s
     d.v_stride = pool_strides3(v_pool)
     d.o_stride = _i64x3(out.stride(0), out.stride(1), out.stride(2))
     d.lse_out = None if lse_out is None else lse_out.data_ptr()
-    pg = make_paging(block_table, k_pool, v_pool)
+    pg = make_paging(block_table, k_pool, v_pool, v_block_table)
     need = pkv_attention_workspace_size(d, H, Hkv, D)
     if need and (workspace is None or workspace.numel() * workspace.element_size() < need):
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)

@@ -39,7 +39,7 @@ def test_struct_sizes_match_header():
     assert ctypes.sizeof(pkv.pkv_segment) == 32
     assert ctypes.sizeof(pkv.pkv_layout) == 40 + 96 + 8
     assert ctypes.sizeof(pkv.pkv_attn_desc) == 40 + 16 + 8 + 96 + 8
-    assert ctypes.sizeof(pkv.pkv_paged_cache) == 8 + 8 + 24
+    assert ctypes.sizeof(pkv.pkv_paged_cache) == 8 + 8 + 24 + 8
 
 
 BASE = 1 << 40   # fake, 16-byte aligned device addresses; never dereferenced
@@ -277,3 +277,6 @@ def test_paged_mla_page_strides_must_match():
     pg = good_paging(page_stride_k=32 * 576, page_stride_v=32 * 576 + 8)
     st = pkv.pkv_suffix_attention_paged(Q, K, K, O, QP, KL, 16, 1, 576, 0.07, d, pg, None, 0, 0)
     assert st == pkv.PKV_ERR_SHAPE and "page_stride_v" in pkv.pkv_last_error()
+    pg = good_paging(page_stride_k=32 * 576, page_stride_v=32 * 576, v_block_table=BASE + 12 * (1 << 32))
+    st = pkv.pkv_suffix_attention_paged(Q, K, K, O, QP, KL, 16, 1, 576, 0.07, d, pg, None, 0, 0)
+    assert st == pkv.PKV_ERR_SHAPE and "v_block_table" in pkv.pkv_last_error()

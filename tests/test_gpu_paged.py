@@ -17,7 +17,7 @@ import pytest
 import torch
 
 import oracle
-from helpers import check_attention_close, check_rotated_keys, dev, host_bits, log, small_workload
+from helpers import check_attention_close, check_rotated_keys, dev, host_bits, log, rope_cache, small_workload
 from paper_2606_17107_amd import pkv, synth
 from test_gpu_attention import assemble_cache
 
@@ -359,3 +359,99 @@ def test_paged_attention_full_gqa8b():
     want, _ = oracle.attention(host_bits(q[0]), host_bits(k[0]), host_bits(v[0]), c["q_pos"].numpy(), w.kv_len,
                                w.scale)
     log("  layer 0", check_attention_close(host_bits(out_p[0]), want))
+
+
+# ---- separate value table: value pages referenced in place -------------------------
+
+def test_paged_splice_separate_v_table():
+    """Keys and values through their own block tables."""
+    L, H, d, n, B, max_pages, P = 2, 4, 128, 200, 32, 12, 30
+    cap = B * max_pages
+    pk, pv = bits((L, P, B, H, d), 40), bits((L, P, B, H, d), 41)
+    sk, sv = bits((L, H, n, d), 42), bits((L, H, n, d), 43)
+    bt_k, bt_v = block_table(1, max_pages, P, 44), block_table(1, max_pages, P, 45)
+    src = (np.arange(n) + 9).astype(np.int32)
+    dst = np.random.default_rng(46).permutation(cap)[:n].astype(np.int32)
+    gk, gv = dev(pk), dev(pv)
+    pkv.reposition_splice_paged(dev(sk), dev(sv), gk, gv, torch.from_numpy(src).cuda(), torch.from_numpy(dst).cuda(),
+                                torch.from_numpy(bt_k).cuda(), 1e4, d, v_block_table=torch.from_numpy(bt_v).cuda())
+    torch.cuda.synchronize()
+    ok, ov = gather(pk, bt_k[0], cap), gather(pv, bt_v[0], cap)
+    oracle.reposition_splice(sk, sv, ok, ov, src, dst, 1e4, d)
+    np.testing.assert_array_equal(gather(host_bits(gv), bt_v[0], cap), ov)
+    check_rotated_keys(gather(host_bits(gk), bt_k[0], cap), ok, 0, d, 0)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_paged_attention_separate_v_table(d):
+    w = small_workload(L=2, H=8, Hkv=2, d=d, theta=1e4, skill=200, dst0=30, ctx=700, n_q=45)
+    c = synth.gqa_case(w, seed=47)
+    q, k, v, q_pos = assemble_cache(w, c)
+    B = 64
+    pk, _, bt_k = paged_inputs(k, None, B, 48)
+    pv, _, bt_v = paged_inputs(v, None, B, 49)
+    want, _ = oracle_out(q, k, v, q_pos, w.kv_len, w.scale, d)
+    for splits in (1, 3):
+        L, nq, H = q.shape[:3]
+        out = torch.zeros(L, nq, H, d, dtype=torch.bfloat16, device="cuda")
+        pkv.suffix_attention_paged(dev(q), dev(pk), dev(pv), out, torch.from_numpy(q_pos).cuda(),
+                                   torch.tensor([w.kv_len], dtype=torch.int32, device="cuda"),
+                                   torch.from_numpy(bt_k).cuda(), w.scale, max_kv_len=w.kv_len, n_splits=splits,
+                                   v_block_table=torch.from_numpy(bt_v).cuda())
+        torch.cuda.synchronize()
+        got = host_bits(out)
+        check_attention_close(got, want)
+        np.testing.assert_array_equal(got, gpu_contiguous(q, k, v, q_pos, w.kv_len, w.scale, d, n_splits=splits))
+
+
+def test_value_pages_remapped_not_copied():
+    """A precompiled skill whose K/V sit in library pages is composed into a new context: its keys
+    are re-rotated into the context's own K pages, its value pages are not copied at all, the
+    context's V table points at the library pages (values are position-free).  Attention then equals
+    the oracle on the cache a full copy would have built."""
+    L, H, Hkv, d, B = 2, 8, 2, 128, 64
+    theta, n_skill, src0, dst0 = 1e4, 256, 0, 320           # skill: 4 whole pages, page-aligned at 320
+    ctx, n_q = 700, 40
+    kv_len = ctx + n_q
+    max_pages = (kv_len + B - 1) // B
+    w = synth.Workload("remap", L, H, Hkv, d, d, theta, d, 0, synth.HALF, "bf16", n_skill, src0, dst0, ctx, n_q,
+                       1 / np.sqrt(d))
+    c = synth.gqa_case(w, seed=50)
+    # logical cache a full copy builds (oracle), and the queries
+    q, k_log, v_log, q_pos = assemble_cache(w, c)
+    # library: the skill's post-RoPE keys (at their source positions) and its values, in pages
+    # P_lib .. P_lib + 3 of both pools
+    skill_k = rope_cache(host_bits(c["skill_k_pre"]), np.arange(src0, src0 + n_skill)[None, None, :], w)
+    skill_v = host_bits(c["skill_v"])
+    n_ctx_pages = max_pages
+    P = n_ctx_pages + n_skill // B + 3
+    lib_pages = np.arange(n_ctx_pages, n_ctx_pages + n_skill // B, dtype=np.int32)
+    perm = np.random.default_rng(51).permutation(n_ctx_pages).astype(np.int32)
+    bt_k = perm[None, :].copy()
+    pk = bits((L, P, B, Hkv, d), 52)
+    pv = bits((L, P, B, Hkv, d), 53)
+    # the context's own pages hold the logical cache except the skill range (K is spliced there below)
+    ctx_k = k_log.copy()
+    ctx_k[:, :, dst0:dst0 + n_skill] = bits((L, Hkv, n_skill, d), 54)   # stale content to be overwritten
+    scatter(pk, bt_k[0], ctx_k)
+    ctx_v = v_log.copy()
+    ctx_v[:, :, dst0:dst0 + n_skill] = bits((L, Hkv, n_skill, d), 55)   # the context's own V pages there: unused
+    scatter(pv, perm, ctx_v)
+    pv[:, lib_pages] = skill_v.transpose(0, 2, 1, 3).reshape(L, n_skill // B, B, Hkv, d)
+    # values: the skill's logical pages map to the library pages
+    bt_v = bt_k.copy()
+    bt_v[0, dst0 // B: (dst0 + n_skill) // B] = lib_pages
+    # keys: re-rotate the skill into the context's K pages (no values moved)
+    gk = dev(pk)
+    pkv.reposition_splice_paged(dev(skill_k), None, gk, None, c["src_pos"].cuda(), c["dst_pos"].cuda(),
+                                torch.from_numpy(bt_k).cuda(), theta, d)
+    out = torch.zeros(L, n_q, H, d, dtype=torch.bfloat16, device="cuda")
+    pkv.suffix_attention_paged(dev(q), gk, dev(pv), out, torch.from_numpy(q_pos).cuda(),
+                               torch.tensor([kv_len], dtype=torch.int32, device="cuda"), torch.from_numpy(bt_k).cuda(),
+                               w.scale, max_kv_len=kv_len, v_block_table=torch.from_numpy(bt_v).cuda())
+    torch.cuda.synchronize()
+    # the spliced keys equal the oracle's splice (one bf16 ulp), the attention the oracle's
+    check_rotated_keys(gather(host_bits(gk), bt_k[0], kv_len)[:, :, dst0:dst0 + n_skill],
+                       k_log[:, :, dst0:dst0 + n_skill], 0, d, 0)
+    want, _ = oracle_out(q, k_log, v_log, q_pos, kv_len, w.scale, d)
+    log("  remapped values", check_attention_close(host_bits(out), want))
