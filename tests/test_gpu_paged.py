@@ -455,3 +455,36 @@ def test_value_pages_remapped_not_copied():
                        k_log[:, :, dst0:dst0 + n_skill], 0, d, 0)
     want, _ = oracle_out(q, k_log, v_log, q_pos, kv_len, w.scale, d)
     log("  remapped values", check_attention_close(host_bits(out), want))
+
+
+def test_paged_ragged_separate_v_tables_window():
+    """Several sequences, each with its own K and V block-table rows, under a sliding window."""
+    H, Hkv, d, L, B, window = 8, 2, 128, 2, 32, 200
+    nqs, kvls = [17, 40, 1, 64], [300, 1000, 77, 513]
+    max_pages = max((kl + B - 1) // B for kl in kvls)
+    P = len(nqs) * max_pages + 5
+    g = synth.Draws(63, "cpu")
+    pk = host_bits(g.normal((L, P, B, Hkv, d)))
+    pv = host_bits(g.normal((L, P, B, Hkv, d)))
+    q = host_bits(g.normal((L, sum(nqs), H, d)))
+    q_pos = np.concatenate([np.arange(kl - n, kl) for n, kl in zip(nqs, kvls)]).astype(np.int32)
+    cu = np.concatenate([[0], np.cumsum(nqs)]).astype(np.int32)
+    bt_k = block_table(len(nqs), max_pages, P, 64)
+    bt_v = block_table(len(nqs), max_pages, P, 65)
+    scale = 1 / np.sqrt(d)
+    for splits in (1, 4):
+        out = torch.zeros(L, sum(nqs), H, d, dtype=torch.bfloat16, device="cuda")
+        pkv.suffix_attention_paged(dev(q), dev(pk), dev(pv), out, torch.from_numpy(q_pos).cuda(),
+                                   torch.tensor(kvls, dtype=torch.int32, device="cuda"), torch.from_numpy(bt_k).cuda(),
+                                   scale, max_kv_len=max(kvls), n_seqs=len(nqs), cu_q=torch.from_numpy(cu).cuda(),
+                                   max_q=max(nqs), n_splits=splits, window=window,
+                                   v_block_table=torch.from_numpy(bt_v).cuda())
+        torch.cuda.synchronize()
+        got = host_bits(out)
+        for s in range(len(nqs)):
+            rows = slice(cu[s], cu[s + 1])
+            ks, vs = gather(pk, bt_k[s], kvls[s]), gather(pv, bt_v[s], kvls[s])
+            for l in range(L):
+                want, _ = oracle.attention(np.ascontiguousarray(q[l, rows]), ks[l], vs[l], q_pos[rows], kvls[s],
+                                           scale, window=window)
+                check_attention_close(got[l, rows], want)

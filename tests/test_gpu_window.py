@@ -114,3 +114,62 @@ def test_window_full_size_gqa8b_sampled():
     got = host_bits(out[layers])
     ref, _ = want(wl, q, k, v, q_pos, w.kv_len, 4096)
     log("  gqa8b window 4096", check_attention_close(got, ref))
+
+
+@pytest.mark.parametrize("window", [40, 300])
+def test_window_ragged_sequences(window):
+    """Windows over several packed sequences (per-sequence query ranges, cache bases and lengths)."""
+    H, Hkv, d, L = 8, 2, 128, 2
+    nqs, kvls = [17, 40, 1, 64], [300, 1000, 77, 513]
+    caps = [kl + 11 for kl in kvls]
+    bases = np.concatenate([[0], np.cumsum(caps)[:-1]]).astype(np.int64)
+    g = synth.Draws(60, "cpu")
+    k = host_bits(g.normal((L, Hkv, int(sum(caps)), d)))
+    v = host_bits(g.normal((L, Hkv, int(sum(caps)), d)))
+    q = host_bits(g.normal((L, sum(nqs), H, d)))
+    q_pos = np.concatenate([np.arange(kl - n, kl) for n, kl in zip(nqs, kvls)]).astype(np.int32)
+    cu = np.concatenate([[0], np.cumsum(nqs)]).astype(np.int32)
+    scale = 1 / np.sqrt(d)
+    for splits in (1, 3):
+        out = torch.zeros(L, sum(nqs), H, d, dtype=torch.bfloat16, device="cuda")
+        pkv.suffix_attention(dev(q), dev(k), dev(v), out, torch.from_numpy(q_pos).cuda(),
+                             torch.tensor(kvls, dtype=torch.int32, device="cuda"), scale, max_kv_len=max(kvls),
+                             n_seqs=len(nqs), cu_q=torch.from_numpy(cu).cuda(),
+                             kv_base=torch.from_numpy(bases).cuda(), max_q=max(nqs), n_splits=splits,
+                             window=window)
+        torch.cuda.synchronize()
+        got = host_bits(out)
+        for s in range(len(nqs)):
+            rows = slice(cu[s], cu[s + 1])
+            ks = slice(bases[s], bases[s] + caps[s])
+            for l in range(L):
+                o, _ = oracle.attention(np.ascontiguousarray(q[l, rows]), np.ascontiguousarray(k[l][:, ks]),
+                                        np.ascontiguousarray(v[l][:, ks]), q_pos[rows], kvls[s], scale,
+                                        window=window)
+                check_attention_close(got[l, rows], o)
+
+
+def test_window_paged_mla():
+    """A windowed MLA layer over a paged latent pool."""
+    L, H, n_q, kv, B, window = 2, 16, 9, 700, 64, 150
+    g = synth.Draws(61, "cpu")
+    q = host_bits(g.normal((L, n_q, H, 576)))
+    rows = host_bits(g.normal((L, 1, kv, 576)))
+    q_pos = np.arange(kv - n_q, kv, dtype=np.int32)
+    scale = 1 / 192 ** 0.5
+    max_pages = (kv + B - 1) // B
+    P = max_pages + 3
+    bt = np.random.default_rng(62).permutation(P)[:max_pages].astype(np.int32)[None, :]
+    pool = host_bits(g.normal((L, P, B, 1, 576)))
+    p = np.arange(kv)
+    pool[:, bt[0, p // B], p % B] = rows.transpose(0, 2, 1, 3)
+    want = np.stack([oracle.attention(q[l], rows[l], rows[l][..., :512], q_pos, kv, scale, window=window)[0]
+                     for l in range(L)])
+    for splits in (1, 2):
+        out = torch.zeros(L, n_q, H, 512, dtype=torch.bfloat16, device="cuda")
+        pd = dev(pool)
+        pkv.suffix_attention_paged(dev(q), pd, pd[..., :512], out, torch.from_numpy(q_pos).cuda(),
+                                   torch.tensor([kv], dtype=torch.int32, device="cuda"), torch.from_numpy(bt).cuda(),
+                                   scale, max_kv_len=kv, variant=pkv.PKV_ATTN_MLA, n_splits=splits, window=window)
+        torch.cuda.synchronize()
+        check_attention_close(host_bits(out), want)
