@@ -18,6 +18,13 @@
  *   - Sec. 5 ("Linear-time TTFT"): the transplant costs a re-rotation pass plus
  *     the suffix; the suffix (or an appended erratum, Sec. 4) attends causally
  *     over the spliced cache.
+ *   - Sec. 8 and Fig. "attention-variant adapters": attention variants that
+ *     keep per-token KV carry the operations over.  Hence
+ *     pkv_reposition_splice_freqs (explicit per-pair frequencies: rescaled RoPE
+ *     schedules, and moving an image by re-rotating only its temporal M-RoPE
+ *     channels), pkv_attn_desc.window (sliding-window layers keep the full
+ *     cache and change only the mask) and the paged entry points (a vLLM-style
+ *     pool of fixed-size pages behind per-sequence block tables).
  *
  * Conventions for every call:
  *   - All tensor and index pointers are DEVICE pointers owned by the caller.
@@ -293,8 +300,9 @@ pkv_status pkv_suffix_attention(const void* q, const void* k_cache, const void* 
 /* Suffix attention over a paged cache: as pkv_suffix_attention with sequence
  * s's slots read through row s of paging->block_table (desc->kv_base must be
  * NULL; desc->cache_slots is the logical capacity, at most max_pages *
- * page_size; k/v strides are {layer, head, in-page slot}).  A 32-key tile
- * always lies within one page.  Block-table entries outside [0, n_pages) are
+ * page_size; k/v strides are {layer, head, in-page slot}; V slots through
+ * paging->v_block_table when it is set).  A 32-key tile always lies within one
+ * page.  Block-table entries outside [0, n_pages) are
  * clamped so that every read stays inside the pool (the slots they map are then
  * undefined).  bf16 only (GQA and MLA).
  * Errors: as pkv_suffix_attention; PKV_ERR_NULL (paging, block table),
