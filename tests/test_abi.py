@@ -280,3 +280,29 @@ def test_paged_mla_page_strides_must_match():
     pg = good_paging(page_stride_k=32 * 576, page_stride_v=32 * 576, v_block_table=BASE + 12 * (1 << 32))
     st = pkv.pkv_suffix_attention_paged(Q, K, K, O, QP, KL, 16, 1, 576, 0.07, d, pg, None, 0, 0)
     assert st == pkv.PKV_ERR_SHAPE and "v_block_table" in pkv.pkv_last_error()
+
+
+def planned_splits(L, H, Hkv, d, dv, total_q, kv, variant=0):
+    """Split count the library picks, read back through the workspace size."""
+    d_ = pkv.pkv_attn_desc()
+    d_.dtype, d_.variant, d_.n_layers, d_.n_seqs, d_.head_dim_v = 0, variant, L, 1, dv
+    d_.total_q, d_.max_q, d_.max_kv_len, d_.n_splits, d_.window = total_q, total_q, kv, 0, 0
+    d_.cache_slots = kv
+    d_.q_stride = pkv._i64x3(total_q * H * d, H * d, d)
+    d_.k_stride = d_.v_stride = pkv._i64x3(Hkv * kv * d, kv * d, d)
+    d_.o_stride = pkv._i64x3(total_q * H * dv, H * dv, dv)
+    n = pkv.pkv_attention_workspace_size(d_, H, Hkv, d)
+    per_split = L * total_q * H * (dv + 1) * 4
+    assert n % per_split == 0
+    return max(1, n // per_split)
+
+
+def test_split_planner_choices():
+    """The planner weighs workgroup rounds over the 256 CUs against the combine pass's traffic:
+    the 8B workload fills the GPU in one round (no split), the 32k prefill splits 3 ways to even out
+    its last round, the MLA workload 5 ways; short caches never split below 256 keys per split."""
+    assert planned_splits(32, 32, 8, 128, 128, 64, 8256) == 1
+    assert planned_splits(28, 28, 4, 128, 128, 1024, 50176) == 3
+    assert planned_splits(27, 16, 1, 576, 512, 128, 32896, variant=1) == 5
+    assert planned_splits(1, 8, 2, 128, 128, 16, 300) == 1
+    assert planned_splits(1, 8, 2, 128, 128, 16, 4096) > 1     # one layer, one KV head pair: split to fill CUs
