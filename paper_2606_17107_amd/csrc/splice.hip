@@ -67,6 +67,12 @@ constexpr int kXcds = 8;
 #define PKV_SPLICE_SEG_TILES 32   // segment mode: token-tile blocks per (row group, segment)
 #endif
 constexpr int kSegTiles = PKV_SPLICE_SEG_TILES;
+#ifndef PKV_SPLICE_SEG_CACHED
+#define PKV_SPLICE_SEG_CACHED 1   // segment mode: cached source loads (segments may share a source)
+#endif
+#ifndef PKV_SPLICE_SEG_FAST
+#define PKV_SPLICE_SEG_FAST 1     // segment mode: segments are the fastest grid axis
+#endif
 
 __device__ inline u32x4 ld16(const char* p) {
 #if PKV_SPLICE_NONTEMPORAL
@@ -75,6 +81,8 @@ __device__ inline u32x4 ld16(const char* p) {
     return *(const u32x4*)p;
 #endif
 }
+// Cached load: segment mode, where several segments may read one source chunk.
+__device__ inline u32x4 ld16_cached(const char* p) { return *(const u32x4*)p; }
 __device__ inline void st16(char* p, u32x4 v) {
 #if PKV_SPLICE_NONTEMPORAL
     __builtin_nontemporal_store(v, (u32x4*)p);
@@ -229,7 +237,12 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
         w_lo = ft.w[__lane_id()];
         w_hi = ft.w[kWave + __lane_id()];
     }
-    const int grp = blockIdx.y;
+    // Grid: token mode (tiles, row groups); segment mode (segments, tile
+    // blocks, row groups) with the segment the fastest axis, so the blocks of
+    // all segments at one (tile block, row) are dispatched together and
+    // segments that read the same source chunk (a shared skill) find it in the
+    // caches.
+    const int grp = SEG && PKV_SPLICE_SEG_FAST ? blockIdx.z : blockIdx.y;
     const uint32_t tid = threadIdx.x;
     const uint32_t tl = g.lanes == 1 ? tid : __umulhi(tid, g.lanes_magic);   // tid / lanes, exact here
     const int lane = (int)(tid - tl * (uint32_t)g.lanes);
@@ -242,7 +255,7 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
     SpliceSegment sg{};
     int64_t n_tok = a.n_tokens;
     if constexpr (SEG) {
-        sg = a.segs[blockIdx.z];
+        sg = a.segs[PKV_SPLICE_SEG_FAST ? blockIdx.x : blockIdx.z];
         n_tok = sg.n_tokens;
     }
 
@@ -297,7 +310,7 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
         // are renumbered to give each XCD one contiguous range of tokens.
         uint32_t tile;
         if constexpr (SEG) {
-            tile = blockIdx.x + step * gridDim.x;
+            tile = PKV_SPLICE_SEG_FAST ? blockIdx.y + step * gridDim.y : blockIdx.x + step * gridDim.x;
             if ((int64_t)tile * g.tok_per_block >= n_tok) break;   // uniform over the block
         } else {
             tile = blockIdx.x;
@@ -342,8 +355,13 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
                 const int l = in ? layer : last_layer, h = in ? head : last_head;
                 doff[u] = ((int64_t)l * d0 + (int64_t)h * d1) * EB;
                 const char* sp = sbase + ((int64_t)l * s0 + (int64_t)h * s1) * EB;
-                va[u] = ld16(sp);
-                vb[u] = ld16(sp + ob);
+                if constexpr (SEG && PKV_SPLICE_SEG_CACHED) {
+                    va[u] = ld16_cached(sp);
+                    vb[u] = ld16_cached(sp + ob);
+                } else {
+                    va[u] = ld16(sp);
+                    vb[u] = ld16(sp + ob);
+                }
                 if (++head == a.n_kv_heads) {
                     head = 0;
                     ++layer;
@@ -501,7 +519,8 @@ hipError_t launch_splice(const SpliceArgs& a, hipStream_t stream) {
 
     for (int b = 0; b < kPairBits; ++b) g.rho[b] = pow(a.theta, -2.0 * (double)(1 << b) / (double)a.rope_dim);
 
-    dim3 grid((unsigned)n_tiles, (unsigned)n_groups, (unsigned)nz);
+    dim3 grid = seg && PKV_SPLICE_SEG_FAST ? dim3((unsigned)nz, (unsigned)n_tiles, (unsigned)n_groups)
+                    : dim3((unsigned)n_tiles, (unsigned)n_groups, (unsigned)nz);
     dim3 block((unsigned)kBlock);
     if (a.elem_bytes == 2)
         return a.rope_style == kHalf ? launch_typed<2, 0>(a, g, grid, block, stream)
