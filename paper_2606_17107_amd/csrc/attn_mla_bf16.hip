@@ -169,13 +169,18 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
         else
             kt = (const char*)(kbase + (int64_t)t0 * kss);
         const uint32_t lds0 = lds_addr_of(dst_stage + wave * 64 * 8);
-        const bool full = t0 + MBN <= loop_end;
+        if (t0 + MBN <= loop_end) {   // full tile: no per-lane adjustment
 #pragma unroll
-        for (int i = 0; i < PER; ++i) {
-            if (i < n_mine) {
-                const int over = t0 + key_of[i] - last_key;
-                const uint32_t back = !full && over > 0 ? (uint32_t)(over * (int32_t)(kss * 2)) : 0u;
-                lds_dma16(lds0 + i * NW * 1024, kt, (uint32_t)src_off[i] - back);
+            for (int i = 0; i < PER; ++i)
+                if (i < n_mine) lds_dma16(lds0 + i * NW * 1024, kt, (uint32_t)src_off[i]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < PER; ++i) {
+                if (i < n_mine) {
+                    const int over = t0 + key_of[i] - last_key;
+                    const uint32_t back = over > 0 ? (uint32_t)(over * (int32_t)(kss * 2)) : 0u;
+                    lds_dma16(lds0 + i * NW * 1024, kt, (uint32_t)src_off[i] - back);
+                }
             }
         }
     };
