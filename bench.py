@@ -166,6 +166,27 @@ class GqaStep:
         if st != 0:
             raise pkv.PkvError(st, pkv.pkv_last_error())
 
+    def layer_calls_setup(self):
+        """Per-layer launches (one call per layer, as a model that interleaves layers makes them):
+        one descriptor for a single layer, the library's own split choice for it, and its workspace."""
+        w = self.w
+        variant = pkv.PKV_ATTN_MLA if w.mla else pkv.PKV_ATTN_GQA
+        self.layer_desc = pkv.make_attn_desc(self.q[:1], self.cache_k[:1], self.v_view[:1], self.out[:1], w.kv_len,
+                                             variant=variant, n_splits=self.desc.n_splits, window=self.window)
+        self.layer_ws_bytes = pkv.pkv_attention_workspace_size(self.layer_desc, w.n_heads, w.n_kv_heads,
+                                                               w.head_dim)
+        self.layer_ws = torch.empty(max(self.layer_ws_bytes, 16), dtype=torch.uint8, device=self.q.device)
+
+    def attention_layer_calls(self, stream):
+        w = self.w
+        for l in range(w.n_layers):
+            st = pkv.pkv_suffix_attention(self.q[l:l + 1], self.cache_k[l:l + 1], self.v_view[l:l + 1],
+                                          self.out[l:l + 1], self.q_pos, self.kv_len, w.n_heads, w.n_kv_heads,
+                                          w.head_dim, w.scale, self.layer_desc, self.layer_ws, self.layer_ws_bytes,
+                                          stream)
+            if st != 0:
+                raise pkv.PkvError(st, pkv.pkv_last_error())
+
     def splice_bytes(self):
         return self.w.splice_bytes()
 
@@ -496,6 +517,35 @@ def main():
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
 
+    # Attention as one launch per layer, as a model that interleaves layers
+    # makes it (a figure beside the layer-batched headline; timed before the
+    # headline so that the headline's launches are the last of the run).
+    layer_calls = None
+    if isinstance(step, GqaStep) and not args.paged:
+        step.layer_calls_setup()
+        t_warm = time.perf_counter()
+        n = 0
+        while n < 3 or time.perf_counter() - t_warm < args.min_warmup_s / 2:
+            step.attention_layer_calls(sh)
+            n += 1
+            if n % 8 == 0:
+                torch.cuda.synchronize()
+        torch.cuda.synchronize()
+        reps = max(5, min(args.steps, 50))
+        lev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in lev:
+            a.record(stream)
+            step.attention_layer_calls(sh)
+            b.record(stream)
+        torch.cuda.synchronize()
+        lt = sorted(a.elapsed_time(b) for a, b in lev)
+        l_ms = sum(lt) / reps
+        layer_calls = {
+            "launches_per_step": w.n_layers, "us": round(l_ms * 1e3, 2), "us_median": round(lt[reps // 2] * 1e3, 2),
+            "us_per_layer": round(l_ms * 1e3 / w.n_layers, 2),
+            "tflops": round(step.attn_flops() / (l_ms * 1e-3) / 1e12, 2),
+            "workspace_bytes": step.layer_ws_bytes}
+
     # Untimed warm-up: the requested steps, continued until at least
     # --min-warmup-s of GPU work has run, so the shader clock has left its
     # idle state before the timed region (a few ms of work is not enough).
@@ -586,6 +636,8 @@ def main():
         "roofline_kernels": [splice_roof, attn_roof],
         "wall_s_timed": round(t_wall, 3),
     }
+    if layer_calls is not None:
+        result["attention_layer_calls"] = layer_calls
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         result["cpu_baseline"] = (cpu_baseline_batched(w, args.cpu_budget) if args.workload == "batched"

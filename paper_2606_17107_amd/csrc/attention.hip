@@ -135,18 +135,38 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
     const int64_t lr = item / a.n_heads;
     const int64_t row = lr % a.total_q;
     const int layer = (int)(lr / a.total_q);
+    // Loads go out CB splits at a time (independent, so their latencies
+    // overlap); the sums still run over s = 0, 1, ... in order.
+    constexpr int CB = 8;
+    const int ns = a.n_splits;
     float mx = -INFINITY;
-    for (int s = 0; s < a.n_splits; ++s) mx = fmaxf(mx, a.ws_lse[(int64_t)s * items + item]);
+    for (int s0 = 0; s0 < ns; s0 += CB) {
+        float l[CB];
+#pragma unroll
+        for (int j = 0; j < CB; ++j) l[j] = s0 + j < ns ? a.ws_lse[(int64_t)(s0 + j) * items + item] : -INFINITY;
+#pragma unroll
+        for (int j = 0; j < CB; ++j) mx = fmaxf(mx, l[j]);
+    }
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     float wsum = 0.f;
     if (mx != -INFINITY) {
-        for (int s = 0; s < a.n_splits; ++s) {
-            const float l = a.ws_lse[(int64_t)s * items + item];
-            if (l == -INFINITY) continue;
-            const float w = __builtin_amdgcn_exp2f(l - mx);
-            const f32x4 v = *(const f32x4*)(a.ws_o + ((int64_t)s * items + item) * dv + c * 4);
-            acc += w * v;
-            wsum += w;
+        for (int s0 = 0; s0 < ns; s0 += CB) {
+            float l[CB];
+            f32x4 v[CB];
+#pragma unroll
+            for (int j = 0; j < CB; ++j) {
+                const bool in = s0 + j < ns;
+                l[j] = in ? a.ws_lse[(int64_t)(s0 + j) * items + item] : -INFINITY;
+                v[j] = in ? *(const f32x4*)(a.ws_o + ((int64_t)(s0 + j) * items + item) * dv + c * 4)
+                          : f32x4{0.f, 0.f, 0.f, 0.f};
+            }
+#pragma unroll
+            for (int j = 0; j < CB; ++j) {
+                if (l[j] == -INFINITY) continue;
+                const float w = __builtin_amdgcn_exp2f(l[j] - mx);
+                acc += w * v[j];
+                wsum += w;
+            }
         }
     }
     const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
@@ -212,11 +232,13 @@ int attention_splits(const AttnArgs& a) {
         return s;
     }
     // Pick the split count that minimises the estimated time: the workgroup
-    // rounds over the CUs times the duration of one workgroup (1/s of the
-    // keys), plus, for s > 1, the split partials written and read back by the
+    // rounds over the CUs times the duration of one workgroup (a fixed cost
+    // for its start-up, first loads and partial write, plus 1/s of the keys),
+    // plus, for s > 1, the split partials written and read back by the
     // combine pass.  Nominal rates (measured on MI355X): the bf16 kernels
-    // sustain about 1.0 PFLOP/s (GQA) and 0.75 PFLOP/s (MLA), the combine
-    // streams at about 5 TB/s.  At least 256 keys per split.
+    // sustain about 1.0 PFLOP/s (GQA) and 0.75 PFLOP/s (MLA), a workgroup's
+    // fixed cost is about 20 us, the combine streams at about 5 TB/s.  At
+    // least 512 keys per split, at most 32 splits.
     const Plan p = make_plan(a, 1);
     const int64_t wgs = (int64_t)p.n_groups * p.rbs;
     const int64_t slots = 256 * (int64_t)wgs_per_cu(a, p);
@@ -226,10 +248,10 @@ int attention_splits(const AttnArgs& a) {
     const double comb_bytes = (double)a.n_layers * a.total_q * a.n_heads * (a.head_dim_v + 1) * 4.0 * 2.0;
     int best = 1;
     double best_t = 1e30;
-    for (int s = 1; s <= 8; ++s) {
-        if (s > 1 && a.max_kv_len / s < 256) break;
+    for (int s = 1; s <= 32; ++s) {
+        if (s > 1 && a.max_kv_len / s < 512) break;
         const double rounds = (double)((wgs * s + slots - 1) / slots);
-        const double t = rounds * (wg_flops / s) / slot_rate + (s > 1 ? s * comb_bytes / 5e12 + 5e-6 : 0.0);
+        const double t = rounds * (20e-6 + (wg_flops / s) / slot_rate) + (s > 1 ? s * comb_bytes / 5e12 + 5e-6 : 0.0);
         if (t < best_t * (1.0 - 1e-9)) {
             best_t = t;
             best = s;
