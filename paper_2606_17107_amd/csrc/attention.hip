@@ -25,7 +25,7 @@ hipError_t launch_attn_mla_bf16(const AttnArgs& a, const Plan& p, dim3 grid, hip
 namespace {
 
 // fp32 GQA kernel: four lanes per row, each holding D/4 channels of q and o;
-// K/V tiles staged in LDS; exact fp32 online softmax per key.
+// K/V tiles of 32 keys staged in LDS; fp32 online softmax, one step per tile.
 template <int D>
 __global__ __launch_bounds__(256) void attn_gqa_f32(AttnArgs a, Plan p) {
     constexpr int BN = 32;
@@ -36,7 +36,8 @@ __global__ __launch_bounds__(256) void attn_gqa_f32(AttnArgs a, Plan p) {
 
     int group, rb;
     if (!decode(p, group, rb)) return;
-    int rest = group;   // one split
+    const int split = group % p.splits;
+    int rest = group / p.splits;
     const int kvh = rest % a.n_kv_heads;
     rest /= a.n_kv_heads;
     const int layer = rest % a.n_layers;
@@ -65,6 +66,8 @@ __global__ __launch_bounds__(256) void attn_gqa_f32(AttnArgs a, Plan p) {
     const int loop_end = max(max(red[0], red[1]), max(red[2], red[3]));
     const int s_min = min(min(red_start[0], red_start[1]), min(red_start[2], red_start[3]));
     const int k_first = s_min == 0x7fffffff ? 0 : s_min / BN * BN;   // tiles before every window are skipped
+    const int k_begin = max(k_first, split * p.chunk);
+    const int k_end = min(loop_end, split * p.chunk + p.chunk);
 
     const float* qrow = (const float*)a.q + (int64_t)layer * a.q_stride[0] +
                         (int64_t)(si.q0 + qi) * a.q_stride[1] + (int64_t)head * a.q_stride[2] + part * DQ;
@@ -79,46 +82,108 @@ __global__ __launch_bounds__(256) void attn_gqa_f32(AttnArgs a, Plan p) {
                          si.base * a.k_stride[2];
     const float* vbase = (const float*)a.v + (int64_t)layer * a.v_stride[0] + (int64_t)kvh * a.v_stride[1] +
                          si.base * a.v_stride[2];
-    for (int t0 = k_first; t0 < loop_end; t0 += BN) {
+    // Tile t+1 is loaded into registers while tile t is consumed from LDS.
+    constexpr int NL = BN * D / 4 / 256;   // 16-byte loads per thread per tensor
+    f32x4 pk[NL], pvv[NL];
+    auto load_tile = [&](int t0) {
+#pragma unroll
+        for (int i = 0; i < NL; ++i) {
+            const int id = tid + i * 256, key = id / (D / 4), c = id % (D / 4);
+            const bool in = t0 + key < k_end;
+            pk[i] = in ? *(const f32x4*)(kbase + (int64_t)(t0 + key) * a.k_stride[2] + c * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+            pvv[i] = in ? *(const f32x4*)(vbase + (int64_t)(t0 + key) * a.v_stride[2] + c * 4)
+                        : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+    };
+    if (k_begin < k_end) load_tile(k_begin);
+    for (int t0 = k_begin; t0 < k_end; t0 += BN) {
         __syncthreads();
-        for (int id = tid; id < BN * D / 4; id += 256) {
-            const int key = id / (D / 4), c = id % (D / 4);
-            f32x4 kv = {0.f, 0.f, 0.f, 0.f}, vv = {0.f, 0.f, 0.f, 0.f};
-            if (t0 + key < loop_end) {
-                kv = *(const f32x4*)(kbase + (int64_t)(t0 + key) * a.k_stride[2] + c * 4);
-                vv = *(const f32x4*)(vbase + (int64_t)(t0 + key) * a.v_stride[2] + c * 4);
-            }
-            *(f32x4*)(k_lds + key * D + c * 4) = kv;
-            *(f32x4*)(v_lds + key * D + c * 4) = vv;
+#pragma unroll
+        for (int i = 0; i < NL; ++i) {
+            const int id = tid + i * 256, key = id / (D / 4), c = id % (D / 4);
+            *(f32x4*)(k_lds + key * D + c * 4) = pk[i];
+            *(f32x4*)(v_lds + key * D + c * 4) = pvv[i];
         }
         __syncthreads();
-        const int n = min(BN, loop_end - t0);
-        for (int kk = 0; kk < n; ++kk) {
-            float s = 0.f;
+        if (t0 + BN < k_end) load_tile(t0 + BN);
+        // The tile's 32 scores first (independent dot products), then one
+        // online-softmax step for the whole tile: its maximum, one rescale of
+        // the running state, 32 independent exponentials and the PV sums.
+        const int n = min(BN, k_end - t0);
+        float sc[BN];
 #pragma unroll
-            for (int c = 0; c < DQ; ++c) s = fmaf(qv[c], k_lds[kk * D + part * DQ + c], s);
-            s += __shfl_xor(s, 1);
-            s += __shfl_xor(s, 2);
-            if (t0 + kk >= row_end || t0 + kk < row_start) continue;   // invisible to this row (uniform over its 4 lanes)
-            const float m_new = fmaxf(m_run, s);
-            const float alpha = expf(m_run - m_new);
-            const float pe = expf(s - m_new);
-            l_run = l_run * alpha + pe;
+        for (int kk = 0; kk < BN; ++kk) {
+            float acc = 0.f;
 #pragma unroll
-            for (int c = 0; c < DQ; ++c) ov[c] = fmaf(ov[c], alpha, pe * v_lds[kk * D + part * DQ + c]);
+            for (int c = 0; c < DQ; c += 4) {
+                const f32x4 kv = *(const f32x4*)(k_lds + kk * D + part * DQ + c);
+                acc = fmaf(qv[c], kv[0], acc);
+                acc = fmaf(qv[c + 1], kv[1], acc);
+                acc = fmaf(qv[c + 2], kv[2], acc);
+                acc = fmaf(qv[c + 3], kv[3], acc);
+            }
+            sc[kk] = acc;
+        }
+        float cmax = -INFINITY;
+#pragma unroll
+        for (int kk = 0; kk < BN; ++kk) {
+            float v = sc[kk] + __shfl_xor(sc[kk], 1);
+            v += __shfl_xor(v, 2);
+            const int key = t0 + kk;
+            // invisible keys (uniform over a row's 4 lanes) drop out
+            v = kk < n && key < row_end && key >= row_start ? v : -INFINITY;
+            sc[kk] = v;
+            cmax = fmaxf(cmax, v);
+        }
+        if (cmax != -INFINITY) {
+            const float m_new = fmaxf(m_run, cmax);
+            const float alpha = expf(m_run - m_new);   // 0 while the running maximum is -inf
+            float psum = 0.f;
+#pragma unroll
+            for (int kk = 0; kk < BN; ++kk) {
+                const float pe = sc[kk] == -INFINITY ? 0.f : expf(sc[kk] - m_new);
+                sc[kk] = pe;
+                psum += pe;
+            }
+            l_run = l_run * alpha + psum;
+#pragma unroll
+            for (int c = 0; c < DQ; c += 4) {
+                f32x4 acc = {ov[c] * alpha, ov[c + 1] * alpha, ov[c + 2] * alpha, ov[c + 3] * alpha};
+#pragma unroll
+                for (int kk = 0; kk < BN; ++kk) {
+                    const f32x4 vv = *(const f32x4*)(v_lds + kk * D + part * DQ + c);
+                    acc[0] = fmaf(sc[kk], vv[0], acc[0]);
+                    acc[1] = fmaf(sc[kk], vv[1], acc[1]);
+                    acc[2] = fmaf(sc[kk], vv[2], acc[2]);
+                    acc[3] = fmaf(sc[kk], vv[3], acc[3]);
+                }
+                ov[c] = acc[0];
+                ov[c + 1] = acc[1];
+                ov[c + 2] = acc[2];
+                ov[c + 3] = acc[3];
+            }
             m_run = m_new;
         }
     }
     if (!row_ok) return;
     const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
     const int64_t row = si.q0 + qi;
-    float* orow = (float*)a.out + (int64_t)layer * a.o_stride[0] + row * a.o_stride[1] +
-                  (int64_t)head * a.o_stride[2] + part * DQ;
+    if (p.splits == 1) {
+        float* orow = (float*)a.out + (int64_t)layer * a.o_stride[0] + row * a.o_stride[1] +
+                      (int64_t)head * a.o_stride[2] + part * DQ;
 #pragma unroll
-    for (int c = 0; c < DQ; ++c) orow[c] = ov[c] * inv;
-    if (a.lse_out && part == 0)
-        a.lse_out[((int64_t)layer * a.total_q + row) * a.n_heads + head] =
-            l_run > 0.f ? m_run + logf(l_run) : -INFINITY;
+        for (int c = 0; c < DQ; ++c) orow[c] = ov[c] * inv;
+        if (a.lse_out && part == 0)
+            a.lse_out[((int64_t)layer * a.total_q + row) * a.n_heads + head] =
+                l_run > 0.f ? m_run + logf(l_run) : -INFINITY;
+    } else {
+        // split partial: normalised output and its log2-sum-exp (the combine's domain)
+        const int64_t item = (((int64_t)split * a.n_layers + layer) * a.total_q + row) * a.n_heads + head;
+        float* wo = a.ws_o + item * D + part * DQ;
+#pragma unroll
+        for (int c = 0; c < DQ; ++c) wo[c] = ov[c] * inv;
+        if (part == 0) a.ws_lse[item] = l_run > 0.f ? (m_run + logf(l_run)) * kLog2e : -INFINITY;
+    }
 }
 
 // Merge split-KV partials: out = sum_s w_s O_s / sum_s w_s with
@@ -170,12 +235,15 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
         }
     }
     const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-    uint16_t* orow = (uint16_t*)a.out + (int64_t)layer * a.o_stride[0] + row * a.o_stride[1] +
-                     (int64_t)head * a.o_stride[2] + c * 4;
-    u32x2 w;
-    w[0] = bf_rne(acc[0] * inv) | (bf_rne(acc[1] * inv) << 16);
-    w[1] = bf_rne(acc[2] * inv) | (bf_rne(acc[3] * inv) << 16);
-    *(u32x2*)orow = w;
+    const int64_t oofs = (int64_t)layer * a.o_stride[0] + row * a.o_stride[1] + (int64_t)head * a.o_stride[2] + c * 4;
+    if (a.dtype == 1) {
+        *(f32x4*)((float*)a.out + oofs) = f32x4{acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv};
+    } else {
+        u32x2 w;
+        w[0] = bf_rne(acc[0] * inv) | (bf_rne(acc[1] * inv) << 16);
+        w[1] = bf_rne(acc[2] * inv) | (bf_rne(acc[3] * inv) << 16);
+        *(u32x2*)((uint16_t*)a.out + oofs) = w;
+    }
     if (a.lse_out && c == 0)
         a.lse_out[item] = wsum > 0.f ? (mx + __log2f(wsum)) * kLn2 : -INFINITY;
 }
@@ -224,7 +292,6 @@ int wgs_per_cu(const AttnArgs& a, const Plan& p) {
 }  // namespace
 
 int attention_splits(const AttnArgs& a) {
-    if (a.dtype == 1) return 1;   // fp32 path: one pass over the keys
     if (a.n_splits > 0) {
         int s = a.n_splits;
         const int max_s = (a.max_kv_len + 63) / 64;
@@ -241,6 +308,15 @@ int attention_splits(const AttnArgs& a) {
     // least 512 keys per split, at most 32 splits.
     const Plan p = make_plan(a, 1);
     const int64_t wgs = (int64_t)p.n_groups * p.rbs;
+    if (a.dtype == 1) {
+        // fp32 path (small problems): one workgroup per CU, at least 64 keys
+        // per split, at most 32 splits.
+        int64_t s = (256 + wgs - 1) / wgs;
+        const int64_t max_s = a.max_kv_len / 64;
+        if (s > max_s) s = max_s;
+        if (s > 32) s = 32;
+        return s < 1 ? 1 : (int)s;
+    }
     const int64_t slots = 256 * (int64_t)wgs_per_cu(a, p);
     const double rate = a.variant == 1 ? 0.75e15 : 1.0e15;
     const double wg_flops = (double)p.BM * a.max_kv_len * (a.head_dim + a.head_dim_v) * 2.0;
@@ -273,14 +349,16 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
     if (n_wg <= 0) return hipSuccess;
     if (n_wg > 0x7fffffff) return hipErrorInvalidValue;
     dim3 grid((unsigned)n_wg), block(256);   // the bf16 launchers set their own block size
+    hipError_t e;
     if (a.dtype == 1) {
         if (a.head_dim == 64)
             hipLaunchKernelGGL((attn_gqa_f32<64>), grid, block, 0, stream, a, p);
         else
             hipLaunchKernelGGL((attn_gqa_f32<128>), grid, block, 0, stream, a, p);
-        return hipGetLastError();
+        e = hipGetLastError();
+    } else {
+        e = a.variant == 1 ? launch_attn_mla_bf16(a, p, grid, stream) : launch_attn_gqa_bf16(a, p, grid, stream);
     }
-    hipError_t e = a.variant == 1 ? launch_attn_mla_bf16(a, p, grid, stream) : launch_attn_gqa_bf16(a, p, grid, stream);
     if (e != hipSuccess || p.splits == 1) return e;
     const int64_t threads = (int64_t)a.n_layers * a.total_q * a.n_heads * (a.head_dim_v / 4);
     dim3 cgrid((unsigned)((threads + 255) / 256));

@@ -173,7 +173,10 @@ def test_workspace_size_and_requirement():
     assert attend(d, ws=WS, wsb=need - 1) == pkv.PKV_ERR_SHAPE
     assert attend(d, ws=WS + 4, wsb=need) == pkv.PKV_ERR_ALIGN
     assert pkv.pkv_attention_workspace_size(attn_desc(n_splits=1), 32, 8, 128) == 0
-    assert pkv.pkv_attention_workspace_size(attn_desc(dtype=1), 32, 8, 128) == 0
+    # fp32: 64 workgroups (2 layers x 8 KV heads x 4 row blocks of 64) split 4 ways to reach the 256 CUs
+    rows = 4 * 2 * 64 * 32
+    assert pkv.pkv_attention_workspace_size(attn_desc(dtype=1), 32, 8, 128) == rows * 128 * 4 + rows * 4
+    assert pkv.pkv_attention_workspace_size(attn_desc(dtype=1, n_splits=1), 32, 8, 128) == 0
     assert pkv.pkv_attention_workspace_size(None, 32, 8, 128) == 0
     assert pkv.pkv_attention_workspace_size(d, 30, 8, 128) == 0
 

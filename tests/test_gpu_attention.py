@@ -63,12 +63,15 @@ def oracle_attention(w, q, k, v, q_pos, kv_len, layers=None, rows=None):
     return np.stack(outs), np.stack(lses)
 
 
-def test_tiny_fp32_config():
+@pytest.mark.parametrize("splits", [0, 1, 3])
+def test_tiny_fp32_config(splits):
+    """The fp32 configuration, in one pass and split over the keys (0: the planner's choice, which
+    splits this two-workgroup problem 8 ways), at fp32 tolerance."""
     w = synth.TINY
     c = synth.gqa_case(w, seed=0)
     q, k, v, q_pos = assemble_cache(w, c)
-    log("tiny fp32 attention")
-    got, lse = gpu_attention(w, q, k, v, q_pos, w.kv_len, lse=True)
+    log("tiny fp32 attention, splits %d" % splits)
+    got, lse = gpu_attention(w, q, k, v, q_pos, w.kv_len, n_splits=splits, lse=True)
     want, want_lse = oracle_attention(w, q, k, v, q_pos, w.kv_len)
     rl2 = np.linalg.norm(got - want) / np.linalg.norm(want)
     assert rl2 <= 1e-5, rl2
