@@ -337,6 +337,16 @@ def cpu_baseline_batched(bw: synth.BatchedWorkload, budget_s: float = 10.0):
     t_splice = time.perf_counter() - t0
     per_pass = sum(2 * 2 * sg["n_tokens"] * bw.n_kv_heads * bw.head_dim * 2 for sg in sq["segs"])
     sample_bytes = per_pass * reps
+    oracle.set_threads(1)
+    reps1, t_splice1 = 0, 0.0
+    try:
+        while reps1 < 1 or (t_splice1 < 0.1 * budget_s and reps1 < reps):
+            t0 = time.perf_counter()
+            run_seq0()
+            t_splice1 += time.perf_counter() - t0
+            reps1 += 1
+    finally:
+        oracle.set_threads(threads)
     q = bits(c["q_pre"][0])[: bw.n_q]
     q_pos = np.arange(sq["ctx"], sq["ctx"] + bw.n_q, dtype=np.int32)
     t0 = time.perf_counter()
@@ -358,6 +368,9 @@ def cpu_baseline_batched(bw: synth.BatchedWorkload, budget_s: float = 10.0):
                   "attention: layer 0, sequence 0, %d of %d queries in %.2f s, scaled to all sequences and layers "
                   "by visible pairs" % (reps, sample_bytes / 1e9, t_splice, n_rows, bw.n_q, t_attn),
         "attention_us_extrapolated": round(attn_us_full, 1),
+        "value_1thread": round(per_pass * reps1 / t_splice1 / 1e9, 4),
+        "sample_1thread": "splice: %d pass(es) over sequence 0's segments of one layer in %.2f s on 1 thread"
+                          % (reps1, t_splice1),
     }
 
 
@@ -393,6 +406,17 @@ def cpu_baseline(w: synth.Workload, budget_s: float = 10.0):
         run_splice(one)
     t_splice = time.perf_counter() - t0
     sample_bytes = w.splice_bytes() / w.n_layers * reps
+    # the same splice on one host thread (a smaller sample: about a tenth of the budget)
+    oracle.set_threads(1)
+    reps1, t_splice1 = 0, 0.0
+    try:
+        while reps1 < 1 or (t_splice1 < 0.1 * budget_s and reps1 < reps):
+            t0 = time.perf_counter()
+            run_splice(one)
+            t_splice1 += time.perf_counter() - t0
+            reps1 += 1
+    finally:
+        oracle.set_threads(threads)
     # attention: layer 0 of the same draws
     q = bits(c1["q_pre"][0])
     k = one["dk"][0]
@@ -422,7 +446,32 @@ def cpu_baseline(w: synth.Workload, budget_s: float = 10.0):
                   "%d pass(es) of layer 0, %d of %d queries over %d slots, in %.2f s, scaled to all layers and queries"
                   % (reps, w.skill_tokens, sample_bytes / 1e9, t_splice, passes, n_rows, w.n_q, w.kv_len, t_attn),
         "attention_us_extrapolated": round(attn_us_full, 1),
+        "value_1thread": round(w.splice_bytes() / w.n_layers * reps1 / t_splice1 / 1e9, 4),
+        "sample_1thread": "splice: %d pass(es) of one layer in %.2f s on 1 thread" % (reps1, t_splice1),
     }
+
+
+def device_copy_gbps(nbytes: int = 1 << 30, reps: int = 10) -> float:
+    """Plain device-to-device copy rate (bytes read + written per second), the practical HBM
+    ceiling the splice is compared against: the better of torch's copy (a DMA-engine copy on ROCm,
+    about 5 TB/s) and an elementwise fp32 kernel that writes its input unchanged (x * 1)."""
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    best = 0.0
+    for f in (lambda: dst.copy_(src), lambda: torch.mul(src, 1.0, out=dst)):
+        for _ in range(3):
+            f()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            f()
+        b.record()
+        torch.cuda.synchronize()
+        best = max(best, 2 * nbytes / (a.elapsed_time(b) / reps * 1e-3) / 1e9)
+    del src, dst
+    torch.cuda.empty_cache()
+    return best
 
 
 def source_hash(files):
@@ -638,6 +687,9 @@ def main():
     }
     if layer_calls is not None:
         result["attention_layer_calls"] = layer_calls
+    cp = device_copy_gbps()
+    result["device_copy_gbps"] = round(cp, 1)
+    result["splice"]["of_device_copy"] = round(splice_gbs / cp, 4)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         result["cpu_baseline"] = (cpu_baseline_batched(w, args.cpu_budget) if args.workload == "batched"
