@@ -333,3 +333,31 @@ def test_full_mla_sampled():
         want, _ = oracle.attention(np.ascontiguousarray(qh), kh, kh[..., :512], c["q_pos"].numpy()[rows], w.kv_len,
                                    w.scale)
         log("  layer", layer, check_attention_close(host_bits(out[layer])[rows], want))
+
+
+@pytest.mark.parametrize("name", ["gqa8b", "long32k", "mla"])
+def test_full_one_layer_per_launch_sampled(name):
+    """The workloads launched one layer at a time, as `bench.py` times them beside the layer-batched
+    launch (the planner then splits 16, 2 and 8 ways): sampled rows of the first and last layer
+    against the oracle."""
+    w = synth.WORKLOADS[name]
+    c = synth.gqa_case(w, seed=3, device="cuda")
+    q, k = c["q_pre"], c["ctx_k"]
+    v = k[..., : w.v_dim] if w.mla else c["ctx_v"]
+    variant = pkv.PKV_ATTN_MLA if w.mla else pkv.PKV_ATTN_GQA
+    out = torch.zeros(w.n_layers, w.n_q, w.n_heads, w.v_dim, dtype=torch.bfloat16, device="cuda")
+    kl = torch.tensor([w.kv_len], dtype=torch.int32, device="cuda")
+    layers = (0, w.n_layers - 1)
+    log("one layer per launch", name, "layers", layers)
+    for l in layers:
+        pkv.suffix_attention(q[l:l + 1], k[l:l + 1], v[l:l + 1], out[l:l + 1], c["q_pos"].cuda(), kl, w.scale,
+                             max_kv_len=w.kv_len, variant=variant)
+    torch.cuda.synchronize()
+    rows = np.unique(np.array([0, 1, w.n_q // 2, w.n_q - 2, w.n_q - 1]))
+    q_pos = c["q_pos"].numpy()
+    for l in layers:
+        qh = np.ascontiguousarray(host_bits(q[l])[rows])
+        kh = host_bits(k[l])
+        vh = kh[..., : w.v_dim] if w.mla else host_bits(v[l])
+        want, _ = oracle.attention(qh, kh, vh, q_pos[rows], w.kv_len, w.scale)
+        log("  layer", l, check_attention_close(host_bits(out[l])[rows], want))
