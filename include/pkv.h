@@ -252,7 +252,8 @@ typedef struct pkv_attn_desc {
     int32_t total_q;        /* query rows per layer over all sequences */
     int32_t max_q;          /* >= the largest per-sequence query count */
     int32_t max_kv_len;     /* >= every kv_len[s]; larger values are clamped to it */
-    int32_t n_splits;       /* KV-length splits; 0 = the library chooses */
+    int32_t n_splits;       /* KV-length splits; 0 = the library chooses (at most 32); an explicit
+                               count above ceil(max_kv_len / 64) is lowered to it */
     int32_t window;         /* 0: full causal attention.  W > 0: sliding window, slot j is visible
                                only if j > q_pos - W as well (the full cache is kept and the mask
                                enforces the window; Sec. 8 sliding-window configuration fix) */
