@@ -111,13 +111,31 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
     // row_start = q_pos - window + 1.
     int qi[QB], head[QB], row_end[QB], row_start[QB];
     bool row_ok[QB];
-    int rmax = 0, rmin = 0x7fffffff, smin = 0x7fffffff, smax = 0;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
         const int m = m0 + (wave * QB + qb) * 32 + j;
         row_ok[qb] = m < M;
         qi[qb] = row_ok[qb] ? m / p.G : 0;
         head[qb] = kvh * p.G + (row_ok[qb] ? m - qi[qb] * p.G : 0);
+    }
+    // Q^T B operands: 8 channels of the row per k-step (loaded first: they do not
+    // depend on the positions, so their latency overlaps the key-range set-up).
+    bf16x8 qf[QB][KS];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+        const uint16_t* qrow = (const uint16_t*)a.q + (int64_t)layer * a.q_stride[0] +
+                               (int64_t)(si.q0 + qi[qb]) * a.q_stride[1] + (int64_t)head[qb] * a.q_stride[2];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            u32x4 v = {0u, 0u, 0u, 0u};
+            if (row_ok[qb]) v = *(const u32x4*)(qrow + ks * 16 + hl * 8);
+            qf[qb][ks] = __builtin_bit_cast(bf16x8, v);
+        }
+    }
+
+    int rmax = 0, rmin = 0x7fffffff, smin = 0x7fffffff, smax = 0;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
         const int qpos = row_ok[qb] ? a.q_pos[si.q0 + qi[qb]] : -1;
         row_end[qb] = row_ok[qb] ? max(0, min(si.kvl, qpos + 1)) : 0;
         row_start[qb] = a.window > 0 && row_ok[qb] ? max(0, qpos - a.window + 1) : 0;
@@ -153,20 +171,6 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
     const int k_begin = max(split_begin, s_min == 0x7fffffff ? 0 : s_min / BN * BN);
     const int loop_end = min(min(si.kvl, split_begin + p.chunk), e_max);
     const int n_tiles = loop_end > k_begin ? (loop_end - k_begin + BN - 1) / BN : 0;
-
-    // Q^T B operands: 8 channels of the row per k-step.
-    bf16x8 qf[QB][KS];
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-        const uint16_t* qrow = (const uint16_t*)a.q + (int64_t)layer * a.q_stride[0] +
-                               (int64_t)(si.q0 + qi[qb]) * a.q_stride[1] + (int64_t)head[qb] * a.q_stride[2];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if (row_ok[qb]) v = *(const u32x4*)(qrow + ks * 16 + hl * 8);
-            qf[qb][ks] = __builtin_bit_cast(bf16x8, v);
-        }
-    }
 
     const uint16_t* kbase = (const uint16_t*)a.k + (int64_t)layer * a.k_stride[0] +
                             (int64_t)kvh * a.k_stride[1] + si.base * a.k_stride[2];

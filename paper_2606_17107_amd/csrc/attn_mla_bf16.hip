@@ -104,6 +104,20 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
     const bool row_ok = m < M;
     const int qi = row_ok ? m / H : 0;
     const int head = row_ok ? m - qi * H : 0;
+    // Q^T operands first: they do not depend on the positions, so their
+    // latency overlaps the key-range set-up.
+    bf16x8 qf[KS];
+    {
+        const uint16_t* qrow = (const uint16_t*)a.q + (int64_t)layer * a.q_stride[0] +
+                               (int64_t)(si.q0 + qi) * a.q_stride[1] + (int64_t)head * a.q_stride[2];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            u32x4 v = {0u, 0u, 0u, 0u};
+            if (row_ok) v = *(const u32x4*)(qrow + (vhalf * KS + ks) * 16 + hl * 8);
+            qf[ks] = __builtin_bit_cast(bf16x8, v);
+        }
+    }
+
     const int qpos = row_ok ? a.q_pos[si.q0 + qi] : -1;
     // Visible keys [row_start, row_end): causal, and with a sliding window
     // also row_start = q_pos - window + 1.
@@ -129,18 +143,6 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
     const int k_begin = max(split_begin, s_min == 0x7fffffff ? 0 : s_min / MBN * MBN);
     const int loop_end = min(min(si.kvl, split_begin + p.chunk), e_max);
     const int n_tiles = loop_end > k_begin ? (loop_end - k_begin + MBN - 1) / MBN : 0;
-
-    bf16x8 qf[KS];
-    {
-        const uint16_t* qrow = (const uint16_t*)a.q + (int64_t)layer * a.q_stride[0] +
-                               (int64_t)(si.q0 + qi) * a.q_stride[1] + (int64_t)head * a.q_stride[2];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if (row_ok) v = *(const u32x4*)(qrow + (vhalf * KS + ks) * 16 + hl * 8);
-            qf[ks] = __builtin_bit_cast(bf16x8, v);
-        }
-    }
 
     const uint16_t* kbase = (const uint16_t*)a.k + (int64_t)layer * a.k_stride[0] + si.base * a.k_stride[2];
     const int64_t kss = a.k_stride[2];
