@@ -128,3 +128,38 @@ def test_sequence_without_slots():
         want, _ = oracle.attention(np.ascontiguousarray(q[0, rows]), np.ascontiguousarray(k[0][:, ks]),
                                    np.ascontiguousarray(v[0][:, ks]), q_pos[rows], kvls[s], 1 / np.sqrt(d))
         check_attention_close(got[0, rows], want)
+
+
+@pytest.mark.parametrize("splits,window", [(0, 0), (0, 150), (5, 150)])
+def test_fp32_ragged_split(splits, window):
+    """fp32 attention over ragged sequences, split over the keys (0: the planner's count) with and
+    without a sliding window, at fp32 tolerance against the oracle."""
+    H, Hkv, d, L = 4, 2, 64, 2
+    nqs, kvls = [7, 16, 3], [530, 300, 700]
+    caps = [kl + 5 for kl in kvls]
+    bases = np.concatenate([[0], np.cumsum(caps)[:-1]]).astype(np.int64)
+    g = synth.Draws(40 + splits + window, "cpu")
+    k = g.normal((L, Hkv, int(sum(caps)), d), torch.float32).numpy()
+    v = g.normal((L, Hkv, int(sum(caps)), d), torch.float32).numpy()
+    q = g.normal((L, sum(nqs), H, d), torch.float32).numpy()
+    q_pos = np.concatenate([np.arange(kl - n, kl) for n, kl in zip(nqs, kvls)]).astype(np.int32)
+    cu = np.concatenate([[0], np.cumsum(nqs)]).astype(np.int32)
+    out = torch.zeros(L, sum(nqs), H, d, dtype=torch.float32, device="cuda")
+    lse = torch.zeros(L, sum(nqs), H, dtype=torch.float32, device="cuda")
+    log("fp32 ragged, splits %d, window %d" % (splits, window))
+    pkv.suffix_attention(torch.from_numpy(q).cuda(), torch.from_numpy(k).cuda(), torch.from_numpy(v).cuda(), out,
+                         torch.from_numpy(q_pos).cuda(), torch.tensor(kvls, dtype=torch.int32, device="cuda"),
+                         1 / np.sqrt(d), max_kv_len=max(kvls), n_seqs=3, cu_q=torch.from_numpy(cu).cuda(),
+                         kv_base=torch.from_numpy(bases).cuda(), max_q=max(nqs), n_splits=splits, lse_out=lse,
+                         window=window)
+    torch.cuda.synchronize()
+    got, lse = out.cpu().numpy().astype(np.float64), lse.cpu().numpy()
+    for l in range(L):
+        for s in range(3):
+            rows = slice(cu[s], cu[s + 1])
+            ks = slice(bases[s], bases[s] + caps[s])
+            want, want_lse = oracle.attention(np.ascontiguousarray(q[l, rows]), np.ascontiguousarray(k[l][:, ks]),
+                                              np.ascontiguousarray(v[l][:, ks]), q_pos[rows], kvls[s],
+                                              1 / np.sqrt(d), window=window)
+            assert np.abs(got[l, rows] - want).max() <= 1e-5
+            np.testing.assert_allclose(lse[l, rows], want_lse, rtol=1e-5, atol=1e-5)
