@@ -285,10 +285,10 @@ def test_paged_mla_page_strides_must_match():
     assert st == pkv.PKV_ERR_SHAPE and "v_block_table" in pkv.pkv_last_error()
 
 
-def planned_splits(L, H, Hkv, d, dv, total_q, kv, variant=0):
+def planned_splits(L, H, Hkv, d, dv, total_q, kv, variant=0, dtype=0):
     """Split count the library picks, read back through the workspace size."""
     d_ = pkv.pkv_attn_desc()
-    d_.dtype, d_.variant, d_.n_layers, d_.n_seqs, d_.head_dim_v = 0, variant, L, 1, dv
+    d_.dtype, d_.variant, d_.n_layers, d_.n_seqs, d_.head_dim_v = dtype, variant, L, 1, dv
     d_.total_q, d_.max_q, d_.max_kv_len, d_.n_splits, d_.window = total_q, total_q, kv, 0, 0
     d_.cache_slots = kv
     d_.q_stride = pkv._i64x3(total_q * H * d, H * d, d)
@@ -315,3 +315,11 @@ def test_split_planner_choices():
     assert planned_splits(1, 8, 2, 128, 128, 16, 300) == 1
     assert planned_splits(1, 8, 2, 128, 128, 16, 1000) == 1    # under 2 x 512 keys: no split
     assert planned_splits(1, 8, 2, 128, 128, 16, 4096) > 1     # one layer, one KV head pair: split to fill CUs
+
+
+def test_split_planner_fp32():
+    """fp32: split until there is about one workgroup per CU, at least 64 keys per split, at most 32."""
+    assert planned_splits(1, 4, 2, 64, 64, 16, 528, dtype=1) == 8       # tiny: 2 workgroups, 528 keys
+    assert planned_splits(1, 4, 2, 64, 64, 16, 100, dtype=1) == 1       # under 2 x 64 keys
+    assert planned_splits(1, 4, 2, 64, 64, 16, 100000, dtype=1) == 32   # capped
+    assert planned_splits(8, 32, 8, 128, 128, 64, 4096, dtype=1) == 1   # 256 workgroups already
