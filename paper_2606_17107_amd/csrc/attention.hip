@@ -4,19 +4,6 @@
 // The bf16 GQA kernel lives in attn_gqa_bf16.hip.
 #include "attn_common.h"
 
-#ifndef PKV_ATTN_SHAPE
-#define PKV_ATTN_SHAPE 1       // bf16 GQA kernel: 0 plain order (64-key tiles), 1 pipelined (32-key tiles)
-#endif
-#ifndef PKV_ATTN_QB
-#define PKV_ATTN_QB 1          // bf16 GQA pipelined kernel: 32-row blocks per wave
-#endif
-#ifndef PKV_MLA_STAGES
-#define PKV_MLA_STAGES 2       // LDS pipeline depth of the MLA kernel
-#endif
-#ifndef PKV_MLA_WAVES
-#define PKV_MLA_WAVES 4        // waves per MLA workgroup (pairs share 32 rows)
-#endif
-
 namespace pkv {
 
 hipError_t launch_attn_gqa_bf16(const AttnArgs& a, const Plan& p, dim3 grid, hipStream_t stream);
@@ -252,21 +239,20 @@ Plan make_plan(const AttnArgs& a, int splits) {
     Plan p;
     p.G = a.n_heads / a.n_kv_heads;
     const int64_t m_rows = (int64_t)a.max_q * p.G;
-    int tile = 64;
+    int tile = 32;
     if (a.variant == 1) {
-        // MLA: wave pairs share 32 rows (each pair: two score-channel halves
-        // and two output halves); 32-key tiles.
+        // MLA: two wave pairs, each sharing 32 rows (two score-channel halves
+        // and two output halves); 32-key tiles in 2 LDS stages.
         p.qb = 1;
-        p.nw = PKV_MLA_WAVES;
-        p.ns = PKV_MLA_STAGES;
-        tile = 32;
-    } else {
-        // bf16 GQA: 4 waves x 32 rows, two workgroups per CU; pipelined over
-        // 32-key tiles in 4 LDS stages, or plain order over 64-key tiles in 2.
-        p.qb = PKV_ATTN_SHAPE == 1 ? PKV_ATTN_QB : 1;
         p.nw = 4;
-        p.ns = PKV_ATTN_SHAPE == 1 ? 4 : 2;
-        tile = PKV_ATTN_SHAPE == 1 ? 32 : 64;
+        p.ns = 2;
+    } else {
+        // bf16 GQA: 4 waves x 32 rows, two workgroups per CU, pipelined over
+        // 32-key tiles in 4 LDS stages.  (The fp32 kernel also uses 32-key
+        // tiles.)
+        p.qb = 1;
+        p.nw = 4;
+        p.ns = 4;
     }
     p.BM = a.dtype == 1 ? 64 : (a.variant == 1 ? p.nw / 2 * 32 : p.nw * 32 * p.qb);
     p.rbs = (int)((m_rows + p.BM - 1) / p.BM);
@@ -282,8 +268,7 @@ Plan make_plan(const AttnArgs& a, int splits) {
 // Workgroups that fit on one CU at once (LDS and register bound).
 int wgs_per_cu(const AttnArgs& a, const Plan& p) {
     if (a.variant == 1) return 1;                     // MLA: 36 KB stages plus the score exchange
-    if (p.qb > 1) return 1;                           // 64 rows per wave: one wave per SIMD (registers)
-    const int tile = p.ns == 4 ? 32 : 64;             // keys per K/V tile
+    const int tile = 32;                              // keys per K/V tile
     const int lds = p.ns * 2 * tile * a.head_dim * 2;
     const int n = (160 * 1024) / lds;
     return n < 1 ? 1 : (n > 2 ? 2 : n);               // two waves per SIMD at most (registers)

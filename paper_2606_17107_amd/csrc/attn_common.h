@@ -140,15 +140,6 @@ __device__ inline uint32_t bf_rne(float f) {
     return u >> 16;
 }
 
-// One 16-byte LDS-DMA load per lane (global_load_lds_dwordx4, saddr form):
-// lane l's 16 bytes at sbase + voff[l] land at LDS byte address lds_addr +
-// 16*l; lds_addr (M0) and sbase are wave-uniform.  Written as inline assembly
-// so that the compiler does not see an LDS write in flight: with the builtin
-// it would wait for every outstanding LDS read (lgkmcnt 0) wherever it needs
-// any one of them.  Completion is tracked by the kernels themselves with
-// explicit vmcnt waits before the barrier that publishes a stage; the memory
-// clobber keeps LDS accesses on their side.  One wait state separates the M0
-// write from the load that reads it.
 // A wave-uniform 64-bit value in scalar registers.  readfirstlane returns a
 // signed int: each half is taken as uint32_t before widening.
 __device__ inline uint64_t uniform_u64(uint64_t v) {
@@ -156,16 +147,27 @@ __device__ inline uint64_t uniform_u64(uint64_t v) {
     const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
     return ((uint64_t)hi << 32) | lo;
 }
-#ifndef PKV_LDS_DMA16
-__device__ inline void lds_dma_asm(uint32_t m0, uint64_t sbase, uint32_t voff) {
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(m0), "v"(voff), "s"(sbase)
-                 : "memory", "m0");
-}
 
 // LDS byte address of a pointer into a __shared__ array (the low 32 bits of
 // its flat address).
 __device__ inline uint32_t lds_addr_of(const void* p) { return (uint32_t)(uintptr_t)p; }
-#endif
+
+// One 16-byte LDS-DMA load per lane (global_load_lds_dwordx4, saddr form):
+// lane l's 16 bytes at sbase + voff[l] land at LDS byte address lds_addr +
+// 16*l; lds_addr (M0) and sbase are wave-uniform.  Written as inline assembly
+// so that the compiler does not see an LDS write in flight: with the builtin
+// it would wait for every outstanding LDS read (lgkmcnt 0) wherever it needs
+// any one of them.  Completion is tracked by the kernels themselves with
+// explicit vmcnt waits before the barrier that publishes a stage; the memory
+// clobber keeps LDS accesses on their side.  M0 is an input operand of the
+// statement ("{m0}" constraint): the compiler writes it right before the
+// load and knows it holds the LDS address, so none of its own uses of M0 can
+// be disturbed.  The s_nop gives the one wait state between that M0 write
+// and the load that reads it.
+__device__ inline void lds_dma_asm(uint32_t m0, uint64_t sbase, uint32_t voff) {
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "{m0}"(m0) : "memory");
+}
+
 __device__ inline void lds_dma16(uint32_t lds_addr, const void* sbase, uint32_t voff) {
     lds_dma_asm((uint32_t)__builtin_amdgcn_readfirstlane(lds_addr), uniform_u64((uint64_t)(uintptr_t)sbase), voff);
 }

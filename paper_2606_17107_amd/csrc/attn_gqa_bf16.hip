@@ -11,9 +11,9 @@
 //     row, so the running max needs one cross-lane step and the running sum
 //     none until the end, and the probabilities P^T already sit in the lane
 //     layout of the B operand of O^T = V^T P^T (no LDS round trip for P).
-//   * K and V tiles of 64 keys stream HBM -> LDS with LDS-DMA loads
-//     (global_load_lds, 16 bytes per lane) through NS stages, so NS-1 tiles
-//     are in flight while one is consumed.  16-byte chunks of a row are
+//   * K and V tiles of 32 keys stream HBM -> LDS with LDS-DMA loads
+//     (global_load_lds, 16 bytes per lane) through 4 stages, so 3 tiles are
+//     in flight while one is consumed.  16-byte chunks of a row are
 //     XOR-swizzled by key (swz_k / swz_v below) to spread LDS banks.
 //   * V stays row-major ([key][channel]) in LDS; the transposed A operand of
 //     the PV product comes from ds_read_b64_tr_b16, with the keys of each
@@ -26,21 +26,12 @@ namespace pkv {
 namespace {
 
 
-#ifndef PKV_ATTN_PRIO
-#define PKV_ATTN_PRIO 2    // wave priority raised over bit 0: the score segment, bit 1: the PV segment
-#endif
-#ifndef PKV_ATTN_PRIO_LEVEL
-#define PKV_ATTN_PRIO_LEVEL 1
-#endif
-#ifndef PKV_ATTN_QB
-#define PKV_ATTN_QB 1      // 32-row blocks per wave of the pipelined kernel
-#endif
-#ifndef PKV_ATTN_AHEAD
-#define PKV_ATTN_AHEAD 3   // LDS operand reads issued this many operands ahead of their MFMA
-#endif
-#ifndef PKV_ATTN_SCHED
-#define PKV_ATTN_SCHED 1   // interleave MFMA, VALU and LDS reads in the pipelined segments
-#endif
+// Kernel shape: 4 waves of 32 rows (one 32-row block each), two workgroups
+// per CU, 32-key tiles through 4 LDS stages (64 KB), software-pipelined.
+constexpr int kQB = 1;       // 32-row blocks per wave
+constexpr int kWaves = 4;
+constexpr int kStages = 4;
+constexpr int kAhead = 3;    // LDS operand reads issued this many operands ahead of their MFMA
 
 // XOR swizzles of a row's 16-byte chunk index by its key.  LDS has 64 banks
 // of 4 bytes (256 bytes per cycle); the rows one read touches must spread
@@ -65,10 +56,11 @@ __device__ inline int swz_v(int key) {
     else return ((key & 3) << 1) | ((key >> 2) & 1);
 }
 
-template <int D, int QB, int NW, int NS, bool PIPE, bool PAGED>
-__global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel(AttnArgs a, Plan p) {
+template <int D, bool PAGED>
+__global__ __launch_bounds__(kWaves * 64, 2) void attn_gqa_bf16_kernel(AttnArgs a, Plan p) {
+    constexpr int QB = kQB, NW = kWaves, NS = kStages;
     constexpr int CH = D / 8;              // 16-byte chunks per row
-    constexpr int BN = PIPE ? 32 : 64;     // keys per tile
+    constexpr int BN = 32;                 // keys per tile
     constexpr int NKB = BN / 32;           // 32-key blocks per tile
     constexpr int KBLK = BN * CH / 64;     // 64-lane LDS-DMA blocks per K (or V) tile
     constexpr int PER = 2 * KBLK / NW;     // LDS-DMA loads per wave per tile (K and V)
@@ -84,8 +76,8 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
     // LDS read (K stages within 48 KB of the block, V stages of the V half).
     __shared__ __attribute__((aligned(16))) uint16_t stage_lds[2 * NS * TE];
     __shared__ int red[NW], red_min[NW], red_start[NW], red_smax[NW];
-    auto kst = [&](int st) -> uint16_t* __attribute__((always_inline)) { return stage_lds + st * TE; };
-    auto vst = [&](int st) -> uint16_t* __attribute__((always_inline)) { return stage_lds + (NS + st) * TE; };
+    auto kst = [&](int st) __attribute__((always_inline)) -> uint16_t* { return stage_lds + st * TE; };
+    auto vst = [&](int st) __attribute__((always_inline)) -> uint16_t* { return stage_lds + (NS + st) * TE; };
 
     int group, rb;
     if (!decode(p, group, rb)) return;
@@ -393,8 +385,8 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
     // tiles before s_max and the tail after them follow in plain order with
     // masks.  Online softmax does not depend on the order of the tiles.
     // Without a window n_lead is 0 and the order is ascending.
-    const int n_lead = PIPE && a.window > 0 ? min(n_tiles, max(0, (s_max - k_begin + BN - 1) / BN)) : 0;
-    const int F = PIPE && sc2 > 0.f ? max(0, min(n_tiles - n_lead, (e_min - (k_begin + n_lead * BN)) / BN)) : 0;
+    const int n_lead = a.window > 0 ? min(n_tiles, max(0, (s_max - k_begin + BN - 1) / BN)) : 0;
+    const int F = sc2 > 0.f ? max(0, min(n_tiles - n_lead, (e_min - (k_begin + n_lead * BN)) / BN)) : 0;
     auto key_of = [&](int i) __attribute__((always_inline)) {
         const int t = i < F ? i + n_lead : (i < F + n_lead ? i - F : i);
         return k_begin + t * BN;
@@ -451,9 +443,7 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
     for (int s = 0; s < NS - 1; ++s)
         if (s < n_tiles) issue(key_of(s), kst(s), vst(s));
 
-    if constexpr (!PIPE) {
-        plain_from(0);
-    } else {
+    {
         // Intra-wave software pipeline over the leading tiles that need no
         // mask (F of them, the same for every wave); tiles are 32 keys (one
         // key block).  With S(t) the raw scores of tile t, iteration t runs
@@ -479,11 +469,11 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
         // Segment 1: nxt = raw scores of key block kbn of the K stage; the
         // probabilities of cur into pb (two 16-key operands per row block).
         // Written as fenced groups of one K operand's MFMAs, their share of
-        // the VALU work and the operand read PKV_ATTN_AHEAD steps ahead, so
+        // the VALU work and the operand read kAhead steps ahead, so
         // the LDS reads stay in flight across MFMAs.
         auto seg1 = [&](const uint16_t* ks_src, int kbn, f32x16 (&cur)[QB], f32x16 (&nxt)[QB],
                         bf16x8 (&pb)[QB][2]) __attribute__((always_inline)) {
-            constexpr int A = PKV_ATTN_AHEAD < KS ? PKV_ATTN_AHEAD : KS;
+            constexpr int A = kAhead < KS ? kAhead : KS;
             constexpr int PER_K = 16 / KS;   // probabilities per k-step and row block
             bf16x8 kop[KS];
 #pragma unroll
@@ -520,7 +510,7 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
         auto seg2 = [&](const uint16_t* vs_src, int kbc, const bf16x8 (&pb)[QB][2], const f32x16 (&nxt)[QB],
                         float (&mx)[QB]) __attribute__((always_inline)) {
             constexpr int NQ = 2 * DB;                 // V operands: two 16-key steps x DB channel blocks
-            constexpr int A = PKV_ATTN_AHEAD < NQ ? PKV_ATTN_AHEAD : NQ;
+            constexpr int A = kAhead < NQ ? kAhead : NQ;
             constexpr int PER_M = 16 / NQ;             // maxima per operand and row block
             constexpr int PER_D = 8 / NQ > 0 ? 8 / NQ : 1;   // sum steps per operand and row block
             bf16x8 vop[NQ];
@@ -590,19 +580,10 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
                              f32x16 (&nxt)[QB]) __attribute__((always_inline)) {
             bf16x8 pb[QB][2];
             float mx[QB];
-#if PKV_ATTN_PRIO & 1
-            __builtin_amdgcn_s_setprio(1);
-#endif
             seg1(ks_next, kbn, cur, nxt, pb);
-#if PKV_ATTN_PRIO & 2
-            __builtin_amdgcn_s_setprio(PKV_ATTN_PRIO_LEVEL);
-#elif PKV_ATTN_PRIO & 1
-            __builtin_amdgcn_s_setprio(0);
-#endif
+            __builtin_amdgcn_s_setprio(1);
             seg2(vs_cur, kbc, pb, nxt, mx);
-#if PKV_ATTN_PRIO & 2
             __builtin_amdgcn_s_setprio(0);
-#endif
             move_max(mx);
         };
 
@@ -745,19 +726,10 @@ __global__ __launch_bounds__(NW * 64, QB == 1 ? 2 : 1) void attn_gqa_bf16_kernel
     }
 }
 
-// Kernel shapes (Plan.ns): 4 waves x 32 rows, two workgroups per CU, and
-//   ns == 4: 32-key tiles, software-pipelined (64 KB of LDS stages);
-//   ns == 2: 64-key tiles, plain order (64 KB of LDS stages).
 template <int D, bool PAGED>
 hipError_t launch_d(const AttnArgs& a, const Plan& p, dim3 grid, hipStream_t stream) {
-    if (p.nw != 4 || p.qb != PKV_ATTN_QB) return hipErrorInvalidValue;
-    if (p.ns == 4)
-        hipLaunchKernelGGL((attn_gqa_bf16_kernel<D, PKV_ATTN_QB, 4, 4, true, PAGED>), grid, dim3(256), 0, stream, a,
-                           p);
-    else if (p.ns == 2 && (!PAGED || a.page_shift >= 6))   // 64-key tiles need pages of 64 slots or more
-        hipLaunchKernelGGL((attn_gqa_bf16_kernel<D, 1, 4, 2, false, PAGED>), grid, dim3(256), 0, stream, a, p);
-    else
-        return hipErrorInvalidValue;
+    if (p.nw != kWaves || p.qb != kQB || p.ns != kStages) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((attn_gqa_bf16_kernel<D, PAGED>), grid, dim3(kWaves * 64), 0, stream, a, p);
     return hipGetLastError();
 }
 

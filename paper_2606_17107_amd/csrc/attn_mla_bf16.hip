@@ -19,9 +19,8 @@
 //     ds_read_b64_tr_b16 (channels 0..511).
 //   * Tiles of 32 keys (36 KB) stream HBM -> LDS by LDS-DMA through NS
 //     stages; chunks XOR-swizzled by the key as in the GQA kernel.
-//   * Four waves (two pairs, 64 rows) per workgroup and two stages by
-//     default; eight waves (two per SIMD) and three stages are selectable at
-//     build time and measured no faster.
+//   * Four waves (two pairs, 64 rows) per workgroup and two LDS stages
+//     (eight waves, two per SIMD, and three stages were measured no faster).
 //   * One wave per SIMD, so every stall is exposed: the operand reads of each
 //     MFMA chain are issued in fenced groups a fixed distance ahead (the
 //     compiler's own order left each MFMA waiting on its read), the second
@@ -36,18 +35,12 @@
 
 #include "attn_common.h"
 
-#ifndef PKV_MLA_STAGES
-#define PKV_MLA_STAGES 2
-#endif
-#ifndef PKV_MLA_WAVES
-#define PKV_MLA_WAVES 4
-#endif
-#ifndef PKV_MLA_AHEAD
-#define PKV_MLA_AHEAD 2   // LDS operand reads issued this many operands ahead of their MFMA
-#endif
-
 namespace pkv {
 namespace {
+
+constexpr int kMlaWaves = 4;    // two wave pairs, 64 rows
+constexpr int kMlaStages = 2;   // LDS stages of 32-key tiles
+constexpr int kMlaAhead = 2;    // LDS operand reads issued this many operands ahead of their MFMA
 
 constexpr int MBN = 32;        // keys per tile
 constexpr int DQK = 576;       // score channels
@@ -64,22 +57,23 @@ constexpr int MCH = DQK / 8;   // 16-byte chunks per row: 72
 // the other half of its 8-chunk group.
 __device__ inline int mswz(int key) { return (((key >> 1) & 1) << 2) | ((key >> 2) & 3); }
 
-template <int NS, int NW, bool PAGED>
-__global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs a, Plan p) {
+template <bool PAGED>
+__global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnArgs a, Plan p) {
+    constexpr int NS = kMlaStages, NW = kMlaWaves;
     constexpr int NBLK = MBN * MCH / 64;       // 64-lane LDS-DMA blocks per tile: 36
     constexpr int PER = (NBLK + NW - 1) / NW;  // blocks of the busiest wave per tile
     constexpr int KS = DQK / 16 / 2;           // k-steps per wave (its half of the channels): 18
     constexpr int DB = DV / 64;                // 32-channel blocks per wave (its half of DV): 8
     constexpr int RPW = NW / 2 * 32;           // rows per workgroup
     constexpr int TE = MBN * DQK;              // elements per tile
-    static_assert(NW == 4 || NW == 8, "four or eight waves (pairs of waves share 32 rows)");
-    static_assert(NS >= 2 && NS <= 4, "2..4 stages");
+    static_assert(NW % 2 == 0, "pairs of waves share 32 rows");
+    static_assert(NS == 2, "two LDS stages");
 
-    __shared__ __attribute__((aligned(16))) uint16_t t0_[TE], t1_[TE], t2_[NS > 2 ? TE : 8], t3_[NS > 3 ? TE : 8];
+    __shared__ __attribute__((aligned(16))) uint16_t t0_[TE], t1_[TE];
     __shared__ int red[NW], red_start[NW];
     // Partial-score exchange: [wave][4 chunks][64 lanes] x 16 bytes.
     __shared__ __attribute__((aligned(16))) float xch[NW * 4 * 64 * 4];
-    auto stage = [&](int st) -> uint16_t* { return st == 0 ? t0_ : st == 1 ? t1_ : st == 2 ? t2_ : t3_; };
+    auto stage = [&](int st) -> uint16_t* { return st == 0 ? t0_ : t1_; };
 
     int group, rb;
     if (!decode(p, group, rb)) return;
@@ -232,7 +226,7 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
         // back to back).
         // Fenced groups: MFMA ks, then the read of the operand A steps ahead,
         // so A LDS round trips stay in flight across the chain.
-        constexpr int A = PKV_MLA_AHEAD < KS ? PKV_MLA_AHEAD : KS;
+        constexpr int A = kMlaAhead < KS ? kMlaAhead : KS;
         auto k_operand = [&](int ks) __attribute__((always_inline)) {
             return __builtin_bit_cast(bf16x8, *(const u32x4*)(ts + kofs[ks & 3] + (ks >> 2) * 64));
         };
@@ -323,7 +317,7 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
         // O^T += V^T P^T: V is channels 0..511 of the same tile; operand
         // q = (16-key step q / DB, channel block q % DB), read A steps ahead.
         constexpr int NQ = 2 * DB;
-        constexpr int AV = PKV_MLA_AHEAD < NQ ? PKV_MLA_AHEAD : NQ;
+        constexpr int AV = kMlaAhead < NQ ? kMlaAhead : NQ;
         static_assert(DB == 8, "one second-half probability per first-half MFMA");
         auto v_operand = [&](int q) __attribute__((always_inline)) {
             const int st = q / DB, db = q % DB;
@@ -427,13 +421,11 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void attn_mla_bf16_kernel(AttnArgs
 }  // namespace
 
 hipError_t launch_attn_mla_bf16(const AttnArgs& a, const Plan& p, dim3 grid, hipStream_t stream) {
-    if (p.nw != PKV_MLA_WAVES || p.ns != PKV_MLA_STAGES || p.BM != PKV_MLA_WAVES / 2 * 32) return hipErrorInvalidValue;
+    if (p.nw != kMlaWaves || p.ns != kMlaStages || p.BM != kMlaWaves / 2 * 32) return hipErrorInvalidValue;
     if (a.block_table)
-        hipLaunchKernelGGL((attn_mla_bf16_kernel<PKV_MLA_STAGES, PKV_MLA_WAVES, true>), grid,
-                           dim3(PKV_MLA_WAVES * 64), 0, stream, a, p);
+        hipLaunchKernelGGL((attn_mla_bf16_kernel<true>), grid, dim3(kMlaWaves * 64), 0, stream, a, p);
     else
-        hipLaunchKernelGGL((attn_mla_bf16_kernel<PKV_MLA_STAGES, PKV_MLA_WAVES, false>), grid,
-                           dim3(PKV_MLA_WAVES * 64), 0, stream, a, p);
+        hipLaunchKernelGGL((attn_mla_bf16_kernel<false>), grid, dim3(kMlaWaves * 64), 0, stream, a, p);
     return hipGetLastError();
 }
 

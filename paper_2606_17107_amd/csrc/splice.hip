@@ -22,12 +22,16 @@
 //     store instruction of a wave covers whole 128-byte lines of
 //     token-contiguous caches.
 //   * omega_i = theta^(-2i/r) is formed in fp64 from seven powers of theta
-//     the host passes in the kernel arguments.  Each thread forms
-//     delta*omega_i in fp64, reduces
-//     it by pi/2 in fp64 (a two-part pi/2, so the reduced angle is accurate to
-//     ~1e-16 for any |delta| < 2^31), and evaluates sin and cos of the reduced
-//     angle in [-pi/4, pi/4] with their Taylor series in fp32 (truncation error
-//     below 2e-9).  The rotation itself is fp32 with one round-to-nearest-even
+//     the host passes in the kernel arguments (relative error about 1e-15
+//     from the products).  Each thread forms delta*omega_i in fp64 and
+//     reduces it by pi/2 with a two-part pi/2.  For the supported
+//     |delta| < 2^24 and omega_i <= 1 the angle is below 2^24, so the error
+//     of the reduced angle is dominated by omega_i's relative error times the
+//     angle (below about 2e-8) plus the rounding of the fp64 product (below
+//     2^24 * 2^-53 = 2^-29): below the fp32 rounding of the sin/cos that
+//     follows, and far below the bf16 spacing (2^-8 relative) of the result.
+//     sin and cos of the reduced angle in [-pi/4, pi/4] are their Taylor
+//     series in fp32 (truncation error below 2e-9).  The rotation itself is fp32 with one round-to-nearest-even
 //     to bf16.  delta == 0 copies bit-exact.
 //   * A block covers a tile of tokens and a few (layer, kv_head) rows: many
 //     small blocks keep the rows in flight at any moment close together in
@@ -44,52 +48,20 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-// Launch-shape constants (tuned on MI355X; overridable at build time).
-#ifndef PKV_SPLICE_UNROLL
-#define PKV_SPLICE_UNROLL 1        // rows whose loads are issued before any is used
-#endif
-#ifndef PKV_SPLICE_ROWS
-#define PKV_SPLICE_ROWS 1          // (layer, kv_head) rows per block
-#endif
-#ifndef PKV_SPLICE_BLOCK
-#define PKV_SPLICE_BLOCK 256       // threads per block
-#endif
-#ifndef PKV_SPLICE_NONTEMPORAL
-#define PKV_SPLICE_NONTEMPORAL 1   // streaming loads/stores: the data is touched once
-#endif
-constexpr int kUnroll = PKV_SPLICE_UNROLL;
-constexpr int kRowsPerBlock = PKV_SPLICE_ROWS;
-constexpr int kBlock = PKV_SPLICE_BLOCK;
+// Launch shape (measured on MI355X).
+constexpr int kUnroll = 1;         // rows whose loads are issued before any is used
+constexpr int kRowsPerBlock = 1;   // (layer, kv_head) rows per block
+constexpr int kBlock = 256;        // threads per block
+constexpr int kSegTiles = 32;      // segment mode: token-tile blocks per (row group, segment)
 constexpr int kHalf = 0;
 constexpr int kWave = 64;
 constexpr int kXcds = 8;
-#ifndef PKV_SPLICE_SEG_TILES
-#define PKV_SPLICE_SEG_TILES 32   // segment mode: token-tile blocks per (row group, segment)
-#endif
-constexpr int kSegTiles = PKV_SPLICE_SEG_TILES;
-#ifndef PKV_SPLICE_SEG_CACHED
-#define PKV_SPLICE_SEG_CACHED 1   // segment mode: cached source loads (segments may share a source)
-#endif
-#ifndef PKV_SPLICE_SEG_FAST
-#define PKV_SPLICE_SEG_FAST 1     // segment mode: segments are the fastest grid axis
-#endif
 
-__device__ inline u32x4 ld16(const char* p) {
-#if PKV_SPLICE_NONTEMPORAL
-    return __builtin_nontemporal_load((const u32x4*)p);
-#else
-    return *(const u32x4*)p;
-#endif
-}
+// Streaming (non-temporal) loads and stores: a single chunk is touched once.
+__device__ inline u32x4 ld16(const char* p) { return __builtin_nontemporal_load((const u32x4*)p); }
 // Cached load: segment mode, where several segments may read one source chunk.
 __device__ inline u32x4 ld16_cached(const char* p) { return *(const u32x4*)p; }
-__device__ inline void st16(char* p, u32x4 v) {
-#if PKV_SPLICE_NONTEMPORAL
-    __builtin_nontemporal_store(v, (u32x4*)p);
-#else
-    *(u32x4*)p = v;
-#endif
-}
+__device__ inline void st16(char* p, u32x4 v) { __builtin_nontemporal_store(v, (u32x4*)p); }
 
 struct Geo {
     int lanes_k, lanes_v, lanes, tok_per_block, rows_per_block;
@@ -242,7 +214,7 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
     // all segments at one (tile block, row) are dispatched together and
     // segments that read the same source chunk (a shared skill) find it in the
     // caches.
-    const int grp = SEG && PKV_SPLICE_SEG_FAST ? blockIdx.z : blockIdx.y;
+    const int grp = SEG ? blockIdx.z : blockIdx.y;
     const uint32_t tid = threadIdx.x;
     const uint32_t tl = g.lanes == 1 ? tid : __umulhi(tid, g.lanes_magic);   // tid / lanes, exact here
     const int lane = (int)(tid - tl * (uint32_t)g.lanes);
@@ -255,7 +227,7 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
     SpliceSegment sg{};
     int64_t n_tok = a.n_tokens;
     if constexpr (SEG) {
-        sg = a.segs[PKV_SPLICE_SEG_FAST ? blockIdx.x : blockIdx.z];
+        sg = a.segs[blockIdx.x];
         n_tok = sg.n_tokens;
     }
 
@@ -310,7 +282,7 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
         // are renumbered to give each XCD one contiguous range of tokens.
         uint32_t tile;
         if constexpr (SEG) {
-            tile = PKV_SPLICE_SEG_FAST ? blockIdx.y + step * gridDim.y : blockIdx.x + step * gridDim.x;
+            tile = blockIdx.y + step * gridDim.y;
             if ((int64_t)tile * g.tok_per_block >= n_tok) break;   // uniform over the block
         } else {
             tile = blockIdx.x;
@@ -355,7 +327,7 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
                 const int l = in ? layer : last_layer, h = in ? head : last_head;
                 doff[u] = ((int64_t)l * d0 + (int64_t)h * d1) * EB;
                 const char* sp = sbase + ((int64_t)l * s0 + (int64_t)h * s1) * EB;
-                if constexpr (SEG && PKV_SPLICE_SEG_CACHED) {
+                if constexpr (SEG) {
                     va[u] = ld16_cached(sp);
                     vb[u] = ld16_cached(sp + ob);
                 } else {
@@ -519,8 +491,8 @@ hipError_t launch_splice(const SpliceArgs& a, hipStream_t stream) {
 
     for (int b = 0; b < kPairBits; ++b) g.rho[b] = pow(a.theta, -2.0 * (double)(1 << b) / (double)a.rope_dim);
 
-    dim3 grid = seg && PKV_SPLICE_SEG_FAST ? dim3((unsigned)nz, (unsigned)n_tiles, (unsigned)n_groups)
-                    : dim3((unsigned)n_tiles, (unsigned)n_groups, (unsigned)nz);
+    dim3 grid = seg ? dim3((unsigned)nz, (unsigned)n_tiles, (unsigned)n_groups)
+                    : dim3((unsigned)n_tiles, (unsigned)n_groups, 1u);
     dim3 block((unsigned)kBlock);
     if (a.elem_bytes == 2)
         return a.rope_style == kHalf ? launch_typed<2, 0>(a, g, grid, block, stream)
