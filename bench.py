@@ -1,16 +1,22 @@
-"""Benchmark of the compose hot path on one MI355X: reposition+splice of a
-precompiled skill's KV into a destination cache, then causal suffix attention
-over the spliced cache (paper Sec. 5: a re-rotation pass plus the suffix).
+"""Benchmark of the compose hot path on one MI355X: reposition+splice of precompiled
+skills' KV into destination caches, then causal suffix attention over the spliced
+caches (paper Sec. 5: the transplant costs a re-rotation pass plus the suffix).
 
-One step = pkv_reposition_splice over every layer and KV head, then
-pkv_suffix_attention over every layer, on synthetic seeded inputs resident in
-HBM.  Default workload: Llama-3-8B-shaped single sequence (32 layers, 32/8
-heads, d 128, RoPE theta 5e5, 4096-token skill spliced at 2000 into 8192
-slots, 64-token suffix over 8256 slots, bf16).
+One step = one reposition+splice launch over every layer and KV head, then one
+suffix-attention launch over every layer, on seeded synthetic inputs resident in
+HBM.  The default run measures all five workloads and prints ONE JSON line whose
+headline is the largest one (batched composition: 16 sequences x 3 skills,
+ragged 256-query suffixes, Llama-3-8B shape); the others (tiny fp32, gqa8b,
+long32k, mla) are nested under "configs" with the same fields.
 
-Prints one JSON line: the splice GB/s as `value`, the attention time and
-TFLOP/s beside it, the roofline of the dominant kernel (timed with HIP events
-on the library's stream), and the CPU oracle timed on a bounded sample.
+Timing: HIP events on the library's stream around each launch.  Every timed
+launch starts cold: a 1 GiB read-modify-write of a flush buffer (beyond the
+256 MB last-level cache) runs before it, outside the events.  Beside the cold
+figures, "warm" repeats the steps back to back (the attention then finds part
+of the splice's writes in the caches), and for the single-sequence workloads
+"attention_layer_calls" launches one layer per call (as a model that
+interleaves its layers does), both from the host and replayed from a HIP
+graph.  The CPU oracle is timed on the host cores beside each workload.
 """
 from __future__ import annotations
 
@@ -32,6 +38,8 @@ METRIC = "KV reposition+splice GB/s; suffix prefix-attention µs and TFLOP/s"
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 FP32_PEAK_TFLOPS = 157.3
+ORDER = ("tiny", "gqa8b", "long32k", "mla", "batched")   # measured in this order; batched is the headline
+FLUSH_BYTES = 1 << 30
 
 
 def log(*a):
@@ -298,12 +306,113 @@ class BatchedStep:
                                                         bw.n_q))
 
 
-def cpu_baseline_batched(bw: synth.BatchedWorkload, budget_s: float = 10.0):
-    """Time the fp64 oracle on a bounded sample of the batched workload: the three
-    segments of sequence 0 for as many single-layer passes as fit in half the
-    budget (scaled to all 48 segments and 32 layers by bytes), and layer 0 of
-    sequence 0's suffix attention for as many queries as fit in the other half
-    (scaled by visible pairs)."""
+# ---- CPU oracle baselines ---------------------------------------------------
+
+def _replicate_layers(one, n_layers):
+    """[1][...] host array -> [n_layers][...] copy (the CPU splice timing streams every layer; the
+    values of one seeded layer are repeated, which does not change the oracle's work)."""
+    import numpy as np
+    return np.ascontiguousarray(np.repeat(one, n_layers, axis=0))
+
+
+def _time_splice(run, budget_s):
+    """Run `run` once, then repeat it while the total stays within budget_s; returns (passes, seconds)."""
+    t0 = time.perf_counter()
+    run()
+    t = time.perf_counter() - t0
+    passes, total = 1, t
+    while total + t <= budget_s:
+        t0 = time.perf_counter()
+        run()
+        total += time.perf_counter() - t0
+        passes += 1
+    return passes, total
+
+
+def cpu_baseline(w: synth.Workload, budget_s: float):
+    """The fp64 oracle on the host cores.  Splice: the full skill over every layer (one seeded layer of
+    draws repeated over the layers), one or more whole passes.  Attention: every layer and query for
+    the tiny and gqa8b workloads; for long32k and mla layer 0 over as many queries as fit in the
+    budget, scaled to all layers and queries by visible (query, key) pairs (labelled extrapolated)."""
+    import numpy as np
+
+    import oracle
+
+    oracle.build(force=False)
+    threads = oracle.max_threads()
+    bits = synth.to_numpy_bits
+    c1 = synth.gqa_case(w, seed=1, layers=1)
+    src, dst = c1["src_pos"].numpy(), c1["dst_pos"].numpy()
+    full = dict(sk=_replicate_layers(bits(c1["skill_k_pre"]), w.n_layers),
+                dk=_replicate_layers(bits(c1["ctx_k"]), w.n_layers),
+                sv=_replicate_layers(bits(c1["skill_v"]), w.n_layers) if not w.mla else None,
+                dv=_replicate_layers(bits(c1["ctx_v"]), w.n_layers) if not w.mla else None)
+
+    def run_full():
+        oracle.reposition_splice(full["sk"], full["sv"], full["dk"], full["dv"], src, dst, w.theta, w.rope_dim,
+                                 w.rope_offset, w.rope_style)
+
+    passes, t_splice = _time_splice(run_full, 0.15 * budget_s)
+    splice_bytes = w.splice_bytes() * passes
+    del full
+    one = dict(sk=bits(c1["skill_k_pre"]), dk=bits(c1["ctx_k"]).copy(),
+               sv=bits(c1["skill_v"]) if not w.mla else None, dv=bits(c1["ctx_v"]).copy() if not w.mla else None)
+    oracle.set_threads(1)
+    try:
+        t0 = time.perf_counter()
+        oracle.reposition_splice(one["sk"], one["sv"], one["dk"], one["dv"], src, dst, w.theta, w.rope_dim,
+                                 w.rope_offset, w.rope_style)
+        t_one1 = time.perf_counter() - t0
+    finally:
+        oracle.set_threads(threads)
+    # attention
+    q_pos = c1["q_pos"].numpy()
+    vis_all = sum(min(w.kv_len, int(q_pos[i]) + 1) for i in range(w.n_q))
+    k0 = bits(c1["ctx_k"])[0]
+    v0 = k0[..., : w.v_dim] if w.mla else bits(c1["ctx_v"])[0]
+    q0 = bits(c1["q_pre"])[0]
+    if w.name in ("tiny", "gqa8b"):
+        # every layer: the draws of the first layer per layer index (same work per layer)
+        t0 = time.perf_counter()
+        for _ in range(w.n_layers):
+            oracle.attention(q0, k0, v0, q_pos, w.kv_len, w.scale)
+        t_attn = time.perf_counter() - t0
+        attn_us, attn_kind = t_attn * 1e6, "measured"
+        attn_sample = "every layer (%d) and query (%d) over %d slots in %.2f s" % (w.n_layers, w.n_q, w.kv_len,
+                                                                                    t_attn)
+    else:
+        t0 = time.perf_counter()
+        oracle.attention(np.ascontiguousarray(q0[:1]), k0, v0, q_pos[:1], w.kv_len, w.scale)
+        t_row = max(time.perf_counter() - t0, 1e-4)
+        n_rows = max(1, min(w.n_q, int(0.6 * budget_s / t_row)))
+        rows = np.linspace(0, w.n_q - 1, n_rows).astype(np.int64)
+        t0 = time.perf_counter()
+        oracle.attention(np.ascontiguousarray(q0[rows]), k0, v0, q_pos[rows], w.kv_len, w.scale)
+        t_attn = time.perf_counter() - t0
+        vis = sum(min(w.kv_len, int(q_pos[i]) + 1) for i in rows)
+        attn_us, attn_kind = t_attn * (vis_all / vis) * w.n_layers * 1e6, "extrapolated"
+        attn_sample = ("layer 0, %d of %d queries (evenly spaced) over %d slots in %.2f s, scaled to all layers "
+                       "and queries by visible pairs" % (n_rows, w.n_q, w.kv_len, t_attn))
+    return {
+        "value": round(splice_bytes / t_splice / 1e9, 4),
+        "unit": "GB/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": "splice: %d full pass(es) over all %d layers (all %d skill tokens, %.3f GB moved) in %.2f s; "
+                  "attention: %s" % (passes, w.n_layers, w.skill_tokens, splice_bytes / 1e9, t_splice, attn_sample),
+        "splice_us": round(t_splice / passes * 1e6, 1),
+        "attention_us": round(attn_us, 1),
+        "attention_kind": attn_kind,
+        "value_1thread": round(w.splice_bytes() / w.n_layers / t_one1 / 1e9, 4),
+        "sample_1thread": "splice: one layer (all skill tokens) in %.3f s on 1 thread" % t_one1,
+    }
+
+
+def cpu_baseline_batched(bw: synth.BatchedWorkload, budget_s: float):
+    """The fp64 oracle on the batched workload: sequence 0's three segments over every layer (one
+    seeded layer of draws repeated over the layers), scaled to all 48 segments by bytes; attention of
+    layer 0, sequence 0 over as many queries as fit, scaled to all sequences and layers by visible
+    pairs (extrapolated)."""
     import numpy as np
 
     import oracle
@@ -313,50 +422,52 @@ def cpu_baseline_batched(bw: synth.BatchedWorkload, budget_s: float = 10.0):
     bits = synth.to_numpy_bits
     plan = synth.batched_plan(bw, 0)
     c = synth.batched_case(bw, plan, seed=1, layers=1)
-    sk, sv = bits(c["skill_k_pre"]), bits(c["skill_v"])
     sq = plan["seqs"][0]
-    seq_k = bits(c["ctx_k"])[:, :, sq["seq_base"]: sq["seq_base"] + sq["kv_len"]].copy()
-    seq_v = bits(c["ctx_v"])[:, :, sq["seq_base"]: sq["seq_base"] + sq["kv_len"]].copy()
+    sk = _replicate_layers(bits(c["skill_k_pre"]), bw.n_layers)
+    sv = _replicate_layers(bits(c["skill_v"]), bw.n_layers)
+    seq_k1 = bits(c["ctx_k"])[:, :, sq["seq_base"]: sq["seq_base"] + sq["kv_len"]]
+    seq_v1 = bits(c["ctx_v"])[:, :, sq["seq_base"]: sq["seq_base"] + sq["kv_len"]]
+    seq_k = _replicate_layers(seq_k1, bw.n_layers)
+    seq_v = _replicate_layers(seq_v1, bw.n_layers)
+    segs = []
+    for sg in sq["segs"]:
+        n = sg["n_tokens"]
+        sl = slice(sg["src_slot0"], sg["src_slot0"] + n)
+        segs.append((np.ascontiguousarray(sk[:, :, sl]), np.ascontiguousarray(sv[:, :, sl]),
+                     np.arange(sg["src_pos0"], sg["src_pos0"] + n, dtype=np.int32),
+                     np.arange(sg["dst_pos0"], sg["dst_pos0"] + n, dtype=np.int32)))
+    del sk, sv
 
     def run_seq0():
-        for sg in sq["segs"]:
-            n = sg["n_tokens"]
-            sl = slice(sg["src_slot0"], sg["src_slot0"] + n)
-            oracle.reposition_splice(np.ascontiguousarray(sk[:, :, sl]), np.ascontiguousarray(sv[:, :, sl]), seq_k,
-                                     seq_v, np.arange(sg["src_pos0"], sg["src_pos0"] + n, dtype=np.int32),
-                                     np.arange(sg["dst_pos0"], sg["dst_pos0"] + n, dtype=np.int32), bw.theta,
-                                     bw.head_dim)
+        for a_k, a_v, s_pos, d_pos in segs:
+            oracle.reposition_splice(a_k, a_v, seq_k, seq_v, s_pos, d_pos, bw.theta, bw.head_dim)
 
-    t0 = time.perf_counter()
-    run_seq0()
-    t_one = time.perf_counter() - t0
-    reps = max(1, min(64, int(0.5 * budget_s / max(t_one, 1e-4))))
-    t0 = time.perf_counter()
-    for _ in range(reps):
-        run_seq0()
-    t_splice = time.perf_counter() - t0
-    per_pass = sum(2 * 2 * sg["n_tokens"] * bw.n_kv_heads * bw.head_dim * 2 for sg in sq["segs"])
-    sample_bytes = per_pass * reps
+    passes, t_splice = _time_splice(run_seq0, 0.2 * budget_s)
+    per_pass = sum(2 * 2 * sg["n_tokens"] * bw.n_layers * bw.n_kv_heads * bw.head_dim * 2 for sg in sq["segs"])
+    sample_bytes = per_pass * passes
     oracle.set_threads(1)
-    reps1, t_splice1 = 0, 0.0
     try:
-        while reps1 < 1 or (t_splice1 < 0.1 * budget_s and reps1 < reps):
-            t0 = time.perf_counter()
-            run_seq0()
-            t_splice1 += time.perf_counter() - t0
-            reps1 += 1
+        t0 = time.perf_counter()
+        a_k, a_v, s_pos, d_pos = segs[0]
+        oracle.reposition_splice(np.ascontiguousarray(a_k[:1]), np.ascontiguousarray(a_v[:1]),
+                                 np.ascontiguousarray(seq_k[:1]), np.ascontiguousarray(seq_v[:1]), s_pos, d_pos,
+                                 bw.theta, bw.head_dim)
+        t_one1 = time.perf_counter() - t0
+        one1_bytes = 2 * 2 * len(s_pos) * bw.n_kv_heads * bw.head_dim * 2
     finally:
         oracle.set_threads(threads)
     q = bits(c["q_pre"][0])[: bw.n_q]
     q_pos = np.arange(sq["ctx"], sq["ctx"] + bw.n_q, dtype=np.int32)
+    k0, v0 = np.ascontiguousarray(seq_k1[0]), np.ascontiguousarray(seq_v1[0])
     t0 = time.perf_counter()
-    oracle.attention(np.ascontiguousarray(q[:1]), seq_k[0], seq_v[0], q_pos[:1], sq["kv_len"], bw.scale)
+    oracle.attention(np.ascontiguousarray(q[:1]), k0, v0, q_pos[:1], sq["kv_len"], bw.scale)
     t_row = max(time.perf_counter() - t0, 1e-4)
-    n_rows = max(1, min(bw.n_q, int(0.5 * budget_s / t_row)))
+    n_rows = max(1, min(bw.n_q, int(0.6 * budget_s / t_row)))
+    rows = np.linspace(0, bw.n_q - 1, n_rows).astype(np.int64)
     t0 = time.perf_counter()
-    oracle.attention(np.ascontiguousarray(q[:n_rows]), seq_k[0], seq_v[0], q_pos[:n_rows], sq["kv_len"], bw.scale)
+    oracle.attention(np.ascontiguousarray(q[rows]), k0, v0, q_pos[rows], sq["kv_len"], bw.scale)
     t_attn = time.perf_counter() - t0
-    vis = sum(min(sq["kv_len"], int(q_pos[i]) + 1) for i in range(n_rows))
+    vis = sum(min(sq["kv_len"], int(q_pos[i]) + 1) for i in rows)
     flops_sample = 4 * bw.head_dim * bw.n_heads * vis
     attn_us_full = t_attn * synth.batched_attn_flops(bw, plan) / flops_sample * 1e6
     return {
@@ -364,92 +475,20 @@ def cpu_baseline_batched(bw: synth.BatchedWorkload, budget_s: float = 10.0):
         "unit": "GB/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": "splice: %d passes over sequence 0's three segments of one layer (%.3f GB moved) in %.2f s; "
-                  "attention: layer 0, sequence 0, %d of %d queries in %.2f s, scaled to all sequences and layers "
-                  "by visible pairs" % (reps, sample_bytes / 1e9, t_splice, n_rows, bw.n_q, t_attn),
-        "attention_us_extrapolated": round(attn_us_full, 1),
-        "value_1thread": round(per_pass * reps1 / t_splice1 / 1e9, 4),
-        "sample_1thread": "splice: %d pass(es) over sequence 0's segments of one layer in %.2f s on 1 thread"
-                          % (reps1, t_splice1),
+        "sample": "splice: %d pass(es) over sequence 0's three segments (%s tokens) on all %d layers (%.3f GB moved) "
+                  "in %.2f s, the rate applied to all 48 segments; attention: layer 0, sequence 0, %d of %d queries "
+                  "(evenly spaced) over %d slots in %.2f s, scaled to all sequences and layers by visible pairs"
+                  % (passes, "/".join(str(sg["n_tokens"]) for sg in sq["segs"]), bw.n_layers, sample_bytes / 1e9,
+                     t_splice, n_rows, bw.n_q, sq["kv_len"], t_attn),
+        "splice_us": round(synth.batched_splice_bytes(bw, plan) / (sample_bytes / t_splice) * 1e6, 1),
+        "attention_us": round(attn_us_full, 1),
+        "attention_kind": "extrapolated",
+        "value_1thread": round(one1_bytes / t_one1 / 1e9, 4),
+        "sample_1thread": "splice: sequence 0's first segment, one layer, in %.3f s on 1 thread" % t_one1,
     }
 
 
-def cpu_baseline(w: synth.Workload, budget_s: float = 10.0):
-    """Time the fp64 oracle on a bounded sample of the same workload on the host cores.
-
-    Splice: the full skill (all tokens) over as many layers as fit in about half
-    the budget.  Attention: layer 0, as many suffix queries as fit in the other
-    half, scaled to all layers and queries by visible (query, key) pairs."""
-    import numpy as np
-
-    import oracle
-
-    oracle.build(force=False)
-    threads = oracle.max_threads()
-    bits = synth.to_numpy_bits
-    # splice: time one layer first, then size the sample
-    c1 = synth.gqa_case(w, seed=1, layers=1)
-    one = dict(sk=bits(c1["skill_k_pre"]), dk=bits(c1["ctx_k"]),
-               sv=bits(c1["skill_v"]) if "skill_v" in c1 else None, dv=bits(c1["ctx_v"]) if "ctx_v" in c1 else None)
-    src, dst = c1["src_pos"].numpy(), c1["dst_pos"].numpy()
-
-    def run_splice(x):
-        oracle.reposition_splice(x["sk"], x["sv"], x["dk"], x["dv"], src, dst, w.theta, w.rope_dim, w.rope_offset,
-                                 w.rope_style)
-
-    t0 = time.perf_counter()
-    run_splice(one)
-    t_one = time.perf_counter() - t0
-    reps = max(1, min(64 * w.n_layers, int(0.5 * budget_s / max(t_one, 1e-4))))
-    t0 = time.perf_counter()
-    for _ in range(reps):
-        run_splice(one)
-    t_splice = time.perf_counter() - t0
-    sample_bytes = w.splice_bytes() / w.n_layers * reps
-    # the same splice on one host thread (a smaller sample: about a tenth of the budget)
-    oracle.set_threads(1)
-    reps1, t_splice1 = 0, 0.0
-    try:
-        while reps1 < 1 or (t_splice1 < 0.1 * budget_s and reps1 < reps):
-            t0 = time.perf_counter()
-            run_splice(one)
-            t_splice1 += time.perf_counter() - t0
-            reps1 += 1
-    finally:
-        oracle.set_threads(threads)
-    # attention: layer 0 of the same draws
-    q = bits(c1["q_pre"][0])
-    k = one["dk"][0]
-    v = k[..., : w.v_dim] if w.mla else one["dv"][0]
-    q_pos = c1["q_pos"].numpy()
-    t0 = time.perf_counter()
-    oracle.attention(np.ascontiguousarray(q[:1]), k, v, q_pos[:1], w.kv_len, w.scale)
-    t_row = max(time.perf_counter() - t0, 1e-4)
-    n_rows = max(1, min(w.n_q, int(0.5 * budget_s / t_row)))
-    # when every query of a layer fits, repeat the layer (up to the layer count) to fill the budget
-    passes = 1
-    if n_rows == w.n_q:
-        passes = max(1, min(w.n_layers, int(0.5 * budget_s / (t_row * w.n_q))))
-    t0 = time.perf_counter()
-    for _ in range(passes):
-        oracle.attention(np.ascontiguousarray(q[:n_rows]), k, v, q_pos[:n_rows], w.kv_len, w.scale)
-    t_attn = time.perf_counter() - t0
-    vis = sum(min(w.kv_len, int(q_pos[i]) + 1) for i in range(n_rows))
-    vis_all = sum(min(w.kv_len, int(q_pos[i]) + 1) for i in range(w.n_q))
-    attn_us_full = t_attn / passes * (vis_all / vis) * w.n_layers * 1e6
-    return {
-        "value": round(sample_bytes / t_splice / 1e9, 4),
-        "unit": "GB/s",
-        "cores": threads,
-        "kind": "oracle",
-        "sample": "splice: %d passes of one layer (all %d skill tokens, %.3f GB moved) in %.2f s; attention: "
-                  "%d pass(es) of layer 0, %d of %d queries over %d slots, in %.2f s, scaled to all layers and queries"
-                  % (reps, w.skill_tokens, sample_bytes / 1e9, t_splice, passes, n_rows, w.n_q, w.kv_len, t_attn),
-        "attention_us_extrapolated": round(attn_us_full, 1),
-        "value_1thread": round(w.splice_bytes() / w.n_layers * reps1 / t_splice1 / 1e9, 4),
-        "sample_1thread": "splice: %d pass(es) of one layer in %.2f s on 1 thread" % (reps1, t_splice1),
-    }
-
+# ---- GPU timing ----------------------------------------------------------------
 
 def device_copy_gbps(nbytes: int = 1 << 30, reps: int = 10) -> float:
     """Plain device-to-device copy rate (bytes read + written per second), the practical HBM
@@ -494,6 +533,8 @@ KERNEL_SOURCES = {   # the sources and compiler options each kernel is built fro
     "attn_mla_bf16": ["paper_2606_17107_amd/csrc/attn_mla_bf16.hip", "paper_2606_17107_amd/csrc/attn_common.h",
                       "paper_2606_17107_amd/csrc/attention.hip", "paper_2606_17107_amd/csrc/pkv_internal.h",
                       "paper_2606_17107_amd/build.py"],
+    "attn_gqa_f32": ["paper_2606_17107_amd/csrc/attention.hip", "paper_2606_17107_amd/csrc/attn_common.h",
+                     "paper_2606_17107_amd/csrc/pkv_internal.h", "paper_2606_17107_amd/build.py"],
 }
 
 
@@ -523,24 +564,213 @@ def copy_calibration():
     print(json.dumps({"copy_calibration_bytes_read": n, "copy_calibration_bytes_written": n, "launches": 3}))
 
 
+class Flush:
+    """A 1 GiB read-modify-write on the timing stream: evicts the 4 MB L2s and the 256 MB last-level
+    cache, so the launch that follows streams its inputs from HBM."""
+
+    def __init__(self):
+        self.buf = torch.zeros(FLUSH_BYTES, dtype=torch.uint8, device="cuda")
+
+    def __call__(self):
+        self.buf.add_(1)
+
+
+def _stats(ms_list):
+    t = sorted(ms_list)
+    return {"us": round(sum(t) / len(t) * 1e3, 2), "us_median": round(t[len(t) // 2] * 1e3, 2),
+            "us_min": round(t[0] * 1e3, 2)}
+
+
+def roofline(kind, kernel, work, ms, bf16=True, workload=None):
+    """Roofline object of one kernel: algorithmic bytes (hbm) or flops (mfma) per launch over its mean
+    event-timed duration."""
+    if kind == "hbm":
+        achieved = work / (ms * 1e-3) / 1e9
+        r = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+             "frac": round(achieved / HBM_PEAK_GBS, 4)}
+    else:
+        peak = BF16_PEAK_TFLOPS if bf16 else FP32_PEAK_TFLOPS
+        achieved = work / (ms * 1e-3) / 1e12
+        r = {"bound": "mfma" if bf16 else "alu", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+             "frac": round(achieved / peak, 4)}
+    r["traffic"] = measured_traffic(kernel, workload) if workload else None
+    r["kernel"] = kernel
+    return r
+
+
+def make_step(name, args):
+    if name == "batched":
+        return synth.BATCHED, BatchedStep(synth.BATCHED, args.splits)
+    w = synth.WORKLOADS[name]
+    return w, GqaStep(w, args.splits, window=args.window, rope=args.rope, page_size=args.paged)
+
+
+def measure(name, args, flush, stream, first):
+    """All GPU figures of one workload."""
+    w, step = make_step(name, args)
+    log("workload", name, "-", step.describe())
+    sh = stream.cuda_stream
+    res = {"workload": step.describe()}
+
+    # Warm-up, cold order: until --warmup steps and --min-warmup-s of work have run (the shader
+    # clock ramps over a few milliseconds of launches; longer on the first workload of the run).
+    min_s = args.min_warmup_s if first else args.min_warmup_s / 2
+    t_warm = time.perf_counter()
+    n_warm = 0
+    while n_warm < args.warmup or time.perf_counter() - t_warm < min_s:
+        flush()
+        step.splice(sh)
+        flush()
+        step.attention(sh)
+        n_warm += 1
+        if n_warm % 8 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    res["warmup_steps_run"] = n_warm
+
+    # Timed steps, every launch cold.
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    for e in ev:
+        flush()
+        e[0].record(stream)
+        step.splice(sh)
+        e[1].record(stream)
+        flush()
+        e[2].record(stream)
+        step.attention(sh)
+        e[3].record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    splice_ms = [e[0].elapsed_time(e[1]) for e in ev]
+    attn_ms = [e[2].elapsed_time(e[3]) for e in ev]
+    s_ms, a_ms = sum(splice_ms) / K, sum(attn_ms) / K
+    bf16 = getattr(w, "dtype", "bf16") == "bf16"
+    s_bytes, a_flops, a_bytes = step.splice_bytes(), step.attn_flops(), step.attn_bytes()
+    ai = a_flops / a_bytes
+    ridge = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+    a_kernel = "attn_mla_bf16" if getattr(w, "mla", False) else ("attn_gqa_bf16" if bf16 else "attn_gqa_f32")
+    wl_key = None if (args.window or args.paged or args.rope != "theta") else name
+    splice_roof = roofline("hbm", "splice_kernel", s_bytes, s_ms, workload=wl_key)
+    if bf16 and ai < ridge:
+        attn_roof = roofline("hbm", a_kernel, a_bytes, a_ms, workload=wl_key)
+    else:
+        attn_roof = roofline("mfma", a_kernel, a_flops, a_ms, bf16=bf16, workload=wl_key)
+    splice_roof["algorithmic_bytes"] = s_bytes
+    attn_roof["algorithmic_bytes"] = a_bytes
+    attn_roof["algorithmic_flops"] = a_flops
+    res.update({
+        "ms_per_step": round(s_ms + a_ms, 4),
+        "wall_ms_per_step_with_flushes": round(t_wall / K * 1e3, 4),
+        "dtype": "bf16" if bf16 else "f32",
+        "splice_bytes": s_bytes, "attention_flops": a_flops, "attention_bytes": a_bytes,
+        "attention_splits": int(step.desc.n_splits) or "auto", "workspace_bytes": step.ws_bytes,
+        "splice": dict(_stats(splice_ms), gbps=round(s_bytes / (s_ms * 1e-3) / 1e9, 1)),
+        "attention": dict(_stats(attn_ms), tflops=round(a_flops / (a_ms * 1e-3) / 1e12, 2),
+                          gbps=round(a_bytes / (a_ms * 1e-3) / 1e9, 1), arith_intensity=round(ai, 1),
+                          bound=attn_roof["bound"]),
+        "roofline": splice_roof if s_ms >= a_ms else attn_roof,
+        "roofline_kernels": [splice_roof, attn_roof],
+    })
+
+    # Warm: the same steps back to back, no flush (the attention finds part of the splice's
+    # writes in the last-level cache).
+    if not args.no_warm:
+        evw = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+        torch.cuda.synchronize()
+        for e in evw:
+            e[0].record(stream)
+            step.splice(sh)
+            e[1].record(stream)
+            step.attention(sh)
+            e[2].record(stream)
+        torch.cuda.synchronize()
+        ws_ = [e[0].elapsed_time(e[1]) for e in evw]
+        wa_ = [e[1].elapsed_time(e[2]) for e in evw]
+        res["warm"] = {"splice": _stats(ws_), "attention": _stats(wa_),
+                       "ms_per_step": round((sum(ws_) + sum(wa_)) / K, 4)}
+
+    # One launch per layer (single-sequence workloads): from the host, and replayed from a graph.
+    if isinstance(step, GqaStep) and not args.paged and not args.no_layer_calls:
+        res["attention_layer_calls"] = layer_calls(step, w, args, flush, stream)
+    return res
+
+
+def layer_calls(step, w, args, flush, stream):
+    sh = stream.cuda_stream
+    step.layer_calls_setup()
+    for _ in range(3):
+        step.attention_layer_calls(sh)
+    torch.cuda.synchronize()
+    reps = max(5, min(args.steps, 20))
+
+    def timed(run):
+        lev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in lev:
+            flush()
+            a.record(stream)
+            run()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) for a, b in lev]
+
+    eager = timed(lambda: step.attention_layer_calls(sh))
+    ref = step.out.clone()
+    # The same calls captured once into a graph (the library allocates nothing and records no
+    # memset, so the calls capture as they are); every replay must reproduce the eager output.
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        step.attention_layer_calls(torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    step.out.zero_()
+    g.replay()
+    torch.cuda.synchronize()
+    if not torch.equal(step.out, ref):
+        raise RuntimeError("graph replay of the per-layer attention calls differs from the eager calls")
+    graph = timed(g.replay)
+    if not torch.equal(step.out, ref):
+        raise RuntimeError("graph replays of the per-layer attention calls differ from the eager calls")
+    del g
+    e_ms, g_ms = sum(eager) / reps, sum(graph) / reps
+    return {"launches_per_step": w.n_layers, "splits": pkv_splits(step), "workspace_bytes": step.layer_ws_bytes,
+            "eager": dict(_stats(eager), us_per_layer=round(e_ms * 1e3 / w.n_layers, 2)),
+            "graph": dict(_stats(graph), us_per_layer=round(g_ms * 1e3 / w.n_layers, 2),
+                          tflops=round(step.attn_flops() / (g_ms * 1e-3) / 1e12, 2),
+                          gbps=round(step.attn_bytes() / (g_ms * 1e-3) / 1e9, 1))}
+
+
+def pkv_splits(step):
+    """Split count the library plans for one layer (from the workspace it asks for)."""
+    w = step.w
+    if step.layer_ws_bytes == 0:
+        return 1
+    per_split = w.n_q * w.n_heads * (w.v_dim + 1) * 4
+    return step.layer_ws_bytes // per_split
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=30)
-    ap.add_argument("--min-warmup-s", type=float, default=0.25,
-                    help="keep warming up until this much wall time has passed (clock ramp)")
-    ap.add_argument("--workload", default="gqa8b", choices=sorted(synth.WORKLOADS) + ["batched"])
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--min-warmup-s", type=float, default=0.5,
+                    help="keep warming up until this much wall time has passed (clock ramp; half of it for "
+                         "every workload after the first)")
+    ap.add_argument("--workload", default="all", choices=["all"] + list(ORDER))
     ap.add_argument("--splits", type=int, default=0, help="KV splits for attention (0 = library choice)")
     ap.add_argument("--rope", default="theta", choices=["theta", "mrope_sectioned", "mrope_interleaved", "llama31"],
                     help="splice frequencies: the theta schedule, or an explicit table through "
                          "pkv_reposition_splice_freqs (M-RoPE temporal move, Llama-3.1 scaling)")
     ap.add_argument("--window", type=int, default=0,
                     help="sliding-window attention over the full cache (0 = causal; single-sequence workloads)")
-    ap.add_argument("--paged", type=int, default=0,
-                    help="page size of a paged KV cache (0 = contiguous cache)")
+    ap.add_argument("--paged", type=int, default=0, help="page size of a paged KV cache (0 = contiguous cache)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=10.0)
+    ap.add_argument("--no-warm", action="store_true", help="skip the back-to-back (warm) figures")
+    ap.add_argument("--no-layer-calls", action="store_true", help="skip the one-launch-per-layer figures")
+    ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle time per workload (about)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 1 GiB device copy (counter calibration for rocprofv3)")
     args = ap.parse_args()
@@ -555,145 +785,57 @@ def main():
         copy_calibration()
         return
     pkv.lib()   # fail loudly if libpkv.so is missing
-
-    if args.workload == "batched":
-        w = synth.BATCHED
-        step = BatchedStep(w, args.splits)
-    else:
-        w = synth.WORKLOADS[args.workload]
-        step = GqaStep(w, args.splits, window=args.window, rope=args.rope, page_size=args.paged)
-    log("workload", w)
+    names = list(ORDER) if args.workload == "all" else [args.workload]
+    if (args.window or args.rope != "theta" or args.paged) and "batched" in names:
+        names = [n for n in names if n != "batched"]
     stream = torch.cuda.current_stream()
-    sh = stream.cuda_stream
-
-    # Attention as one launch per layer, as a model that interleaves layers
-    # makes it (a figure beside the layer-batched headline; timed before the
-    # headline so that the headline's launches are the last of the run).
-    layer_calls = None
-    if isinstance(step, GqaStep) and not args.paged:
-        step.layer_calls_setup()
-        t_warm = time.perf_counter()
-        n = 0
-        while n < 3 or time.perf_counter() - t_warm < args.min_warmup_s / 2:
-            step.attention_layer_calls(sh)
-            n += 1
-            if n % 8 == 0:
-                torch.cuda.synchronize()
+    flush = Flush()
+    configs = {}
+    t_gpu = time.perf_counter()
+    for i, name in enumerate(names):
+        configs[name] = measure(name, args, flush, stream, first=(i == 0))
         torch.cuda.synchronize()
-        reps = max(5, min(args.steps, 50))
-        lev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
-        for a, b in lev:
-            a.record(stream)
-            step.attention_layer_calls(sh)
-            b.record(stream)
-        torch.cuda.synchronize()
-        lt = sorted(a.elapsed_time(b) for a, b in lev)
-        l_ms = sum(lt) / reps
-        layer_calls = {
-            "launches_per_step": w.n_layers, "us": round(l_ms * 1e3, 2), "us_median": round(lt[reps // 2] * 1e3, 2),
-            "us_per_layer": round(l_ms * 1e3 / w.n_layers, 2),
-            "tflops": round(step.attn_flops() / (l_ms * 1e-3) / 1e12, 2),
-            "workspace_bytes": step.layer_ws_bytes}
-
-    # Untimed warm-up: the requested steps, continued until at least
-    # --min-warmup-s of GPU work has run, so the shader clock has left its
-    # idle state before the timed region (a few ms of work is not enough).
-    t_warm = time.perf_counter()
-    n_warm = 0
-    while n_warm < args.warmup or time.perf_counter() - t_warm < args.min_warmup_s:
-        step.splice(sh)
-        step.attention(sh)
-        n_warm += 1
-        if n_warm % 16 == 0:
-            torch.cuda.synchronize()
-    torch.cuda.synchronize()
-
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    start.record(stream)
-    for i in range(args.steps):
-        ev[i][0].record(stream)
-        step.splice(sh)
-        ev[i][1].record(stream)
-        step.attention(sh)
-        ev[i][2].record(stream)
-    stop.record(stream)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    total_ms = start.elapsed_time(stop)
-    splice_t = sorted(e[0].elapsed_time(e[1]) for e in ev)
-    attn_t = sorted(e[1].elapsed_time(e[2]) for e in ev)
-    # The mean launch duration is the figure rocprofv3's per-kernel average reports; median and min beside it.
-    splice_ms = sum(splice_t) / args.steps
-    attn_ms = sum(attn_t) / args.steps
-    ms_per_step = total_ms / args.steps
-
-    splice_gbs = step.splice_bytes() / (splice_ms * 1e-3) / 1e9
-    attn_tflops = step.attn_flops() / (attn_ms * 1e-3) / 1e12
-    attn_gbs = step.attn_bytes() / (attn_ms * 1e-3) / 1e9
-    ai = step.attn_flops() / step.attn_bytes()
-    ridge = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
-    attn_bound = "hbm" if ai < ridge else "mfma"
-    if attn_bound == "hbm":
-        attn_roof = {"bound": "hbm", "achieved": round(attn_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(attn_gbs / HBM_PEAK_GBS, 4), "traffic": None}
-    else:
-        attn_roof = {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": BF16_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4), "traffic": None}
-    splice_roof = {"bound": "hbm", "achieved": round(splice_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                   "frac": round(splice_gbs / HBM_PEAK_GBS, 4), "traffic": None}
-    splice_roof["kernel"] = "splice_kernel"
-    mla = getattr(w, "mla", False)
-    attn_roof["kernel"] = "attn_gqa_bf16" if not mla else "attn_mla_bf16"
-    splice_roof["traffic"] = measured_traffic("splice_kernel", w.name)
-    attn_roof["traffic"] = measured_traffic(attn_roof["kernel"], w.name)
-    splice_roof["algorithmic_bytes"] = step.splice_bytes()
-    attn_roof["algorithmic_bytes"] = step.attn_bytes()
-    attn_roof["algorithmic_flops"] = step.attn_flops()
-    dominant = splice_roof if splice_ms >= attn_ms else attn_roof
-
+        torch.cuda.empty_cache()
+    t_gpu = time.perf_counter() - t_gpu
+    cp = device_copy_gbps()
+    for r in configs.values():
+        r["splice"]["of_device_copy"] = round(r["splice"]["gbps"] / cp, 4)
+    if not args.no_cpu_baseline:
+        for name in names:
+            log("timing the CPU oracle:", name)
+            configs[name]["cpu_baseline"] = (cpu_baseline_batched(synth.BATCHED, args.cpu_budget) if name == "batched"
+                                             else cpu_baseline(synth.WORKLOADS[name], args.cpu_budget))
+    head_name = names[-1]
+    head = configs[head_name]
     result = {
         "metric": METRIC,
-        "value": round(splice_gbs, 1),
+        "value": head["splice"]["gbps"],
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "warmup_steps_run": n_warm,
-        "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "dtype": head["dtype"],
         "data": "synthetic",
-        "config": {
-            "workload": step.describe(),
-            "splice_bytes": step.splice_bytes(),
-            "attention_flops": step.attn_flops(),
-            "attention_bytes": step.attn_bytes(),
-            "attention_splits": int(step.desc.n_splits) or "auto",
-            "workspace_bytes": step.ws_bytes,
-        },
-        "splice": {"us": round(splice_ms * 1e3, 2), "us_median": round(splice_t[len(splice_t) // 2] * 1e3, 2),
-                   "us_min": round(splice_t[0] * 1e3, 2), "gbps": round(splice_gbs, 1)},
-        "attention": {"us": round(attn_ms * 1e3, 2), "us_median": round(attn_t[len(attn_t) // 2] * 1e3, 2),
-                      "us_min": round(attn_t[0] * 1e3, 2), "tflops": round(attn_tflops, 2),
-                      "gbps": round(attn_gbs, 1), "arith_intensity": round(ai, 1), "bound": attn_bound},
-        "roofline": dominant,
-        "roofline_kernels": [splice_roof, attn_roof],
-        "wall_s_timed": round(t_wall, 3),
+        "config": {"workload": head["workload"], "name": head_name, "splice_bytes": head["splice_bytes"],
+                   "attention_flops": head["attention_flops"], "attention_bytes": head["attention_bytes"],
+                   "attention_splits": head["attention_splits"], "workspace_bytes": head["workspace_bytes"],
+                   "timing": "HIP events per launch, every timed launch after a 1 GiB flush (cold)"},
+        "splice": head["splice"],
+        "attention": head["attention"],
+        "roofline": head["roofline"],
+        "roofline_kernels": head["roofline_kernels"],
+        "device_copy_gbps": round(cp, 1),
+        "gpu_wall_s": round(t_gpu, 2),
+        "configs": configs,
     }
-    if layer_calls is not None:
-        result["attention_layer_calls"] = layer_calls
-    cp = device_copy_gbps()
-    result["device_copy_gbps"] = round(cp, 1)
-    result["splice"]["of_device_copy"] = round(splice_gbs / cp, 4)
-    if not args.no_cpu_baseline:
-        log("timing the CPU oracle on a bounded sample")
-        result["cpu_baseline"] = (cpu_baseline_batched(w, args.cpu_budget) if args.workload == "batched"
-                                  else cpu_baseline(w, args.cpu_budget))
+    if "cpu_baseline" in head:
+        result["cpu_baseline"] = head["cpu_baseline"]
+    if "warm" in head:
+        result["warm"] = head["warm"]
     print(json.dumps(result), flush=True)
 
 

@@ -283,7 +283,9 @@ size_t pkv_attention_workspace_size(const pkv_attn_desc* desc, int32_t n_q_heads
  * q is post-RoPE (q_pos only masks).  bf16: QK^T and PV on bf16 MFMA with fp32
  * accumulation, softmax statistics in fp32, probabilities rounded to bf16
  * before PV, output rounded to bf16.  fp32: fp32 FMA throughout.  A row with no
- * visible slot is written as zeros.  q_pos: device int32 [total_q]; kv_len:
+ * visible slot is written as zeros.  Rows of out (and lse_out) that no
+ * sequence owns (outside every [cu_q[s], cu_q[s+1]) range) are not written,
+ * whatever the split count.  q_pos: device int32 [total_q]; kv_len:
  * device int32 [n_seqs].  workspace: device memory of at least
  * pkv_attention_workspace_size() bytes (may be NULL when that is 0), owned by
  * the caller, contents scratch.

@@ -174,19 +174,32 @@ __global__ __launch_bounds__(256) void attn_gqa_f32(AttnArgs a, Plan p) {
 }
 
 // Merge split-KV partials: out = sum_s w_s O_s / sum_s w_s with
-// w_s = 2^(lse_s - max lse).  One thread per 4 output channels.
+// w_s = 2^(lse_s - max lse).  One thread per 4 output channels of one
+// (layer, sequence, query, head); rows that no sequence owns (outside every
+// cu_q range) are left untouched, as the one-pass kernels leave them.
 __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
     const int dv = a.head_dim_v;
     const int chunks = dv / 4;
-    const int64_t items = (int64_t)a.n_layers * a.total_q * a.n_heads;
+    const int64_t items = (int64_t)a.n_layers * a.total_q * a.n_heads;   // partial records per split
     const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t item = gid / chunks;
+    const int64_t slot = gid / chunks;    // (layer, sequence, query of the sequence, head)
     const int c = (int)(gid % chunks);
-    if (item >= items) return;
-    const int head = (int)(item % a.n_heads);
-    const int64_t lr = item / a.n_heads;
-    const int64_t row = lr % a.total_q;
-    const int layer = (int)(lr / a.total_q);
+    if (slot >= (int64_t)a.n_layers * a.n_seqs * a.max_q * a.n_heads) return;
+    const int head = (int)(slot % a.n_heads);
+    int64_t rest = slot / a.n_heads;
+    const int qi = (int)(rest % a.max_q);
+    rest /= a.max_q;
+    const int seq = (int)(rest % a.n_seqs);
+    const int layer = (int)(rest / a.n_seqs);
+    int q0 = 0, nq = a.total_q;
+    if (a.cu_q) {
+        q0 = a.cu_q[seq];
+        nq = a.cu_q[seq + 1] - q0;
+    }
+    if (q0 < 0 || nq < 0 || (int64_t)q0 + nq > a.total_q) nq = 0;   // as seq_info
+    if (qi >= nq) return;
+    const int64_t row = q0 + qi;
+    const int64_t item = ((int64_t)layer * a.total_q + row) * a.n_heads + head;
     // Loads go out CB splits at a time (independent, so their latencies
     // overlap); the sums still run over s = 0, 1, ... in order.
     constexpr int CB = 8;
@@ -345,7 +358,8 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
         e = a.variant == 1 ? launch_attn_mla_bf16(a, p, grid, stream) : launch_attn_gqa_bf16(a, p, grid, stream);
     }
     if (e != hipSuccess || p.splits == 1) return e;
-    const int64_t threads = (int64_t)a.n_layers * a.total_q * a.n_heads * (a.head_dim_v / 4);
+    const int64_t threads = (int64_t)a.n_layers * a.n_seqs * a.max_q * a.n_heads * (a.head_dim_v / 4);
+    if (threads == 0) return hipSuccess;
     dim3 cgrid((unsigned)((threads + 255) / 256));
     hipLaunchKernelGGL(attn_combine, cgrid, block, 0, stream, a);
     return hipGetLastError();

@@ -139,6 +139,17 @@ def _ptr(t) -> Optional[int]:
     return t.data_ptr()
 
 
+def _keep_until_done(t: Optional[torch.Tensor], stream) -> None:
+    """A workspace allocated here is freed when the call returns; when the kernels run on a stream other
+    than torch's current one, tell the caching allocator that stream still uses it."""
+    if t is None or stream is None:
+        return
+    if isinstance(stream, int):
+        stream = torch.cuda.ExternalStream(stream)
+    if stream != torch.cuda.current_stream(t.device):
+        t.record_stream(stream)
+
+
 def _stream(stream) -> Optional[int]:
     if stream is None:
         return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else None
@@ -336,6 +347,7 @@ def suffix_attention(q, k_cache, v_cache, out, q_pos, kv_len, scale, max_kv_len,
     need = pkv_attention_workspace_size(desc, H, Hkv, D)
     if need and (workspace is None or workspace.numel() * workspace.element_size() < need):
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+        _keep_until_done(workspace, stream)
     _check(pkv_suffix_attention(q, k_cache, v_cache, out, q_pos, kv_len, H, Hkv, D, scale, desc,
                                 workspace, need, stream))
 
@@ -414,5 +426,6 @@ def suffix_attention_paged(q, k_pool, v_pool, out, q_pos, kv_len, block_table, s
     need = pkv_attention_workspace_size(d, H, Hkv, D)
     if need and (workspace is None or workspace.numel() * workspace.element_size() < need):
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+        _keep_until_done(workspace, stream)
     _check(pkv_suffix_attention_paged(q, k_pool, v_pool, out, q_pos, kv_len, H, Hkv, D, scale, d, pg, workspace,
                                       need, stream))

@@ -12,7 +12,8 @@ import pytest
 import torch
 
 import oracle
-from helpers import bits_to_f64, check_attention_close, dev, host_bits, log, rope_cache, rope_queries, small_workload
+from helpers import (Guarded, bits_to_f64, check_attention_close, dev, guarded_attention, host_bits, log, rope_cache,
+                     rope_queries, small_workload)
 from paper_2606_17107_amd import pkv, synth
 
 pytestmark = pytest.mark.gpu
@@ -222,18 +223,29 @@ def test_determinism():
 
 # ---- full-size workloads, sampled against the oracle ---------------------------
 
-def full_gqa(w, layers, rows, seed=0):
+def full_gqa(w, layers, rows, seed=0, q_scale=1, needle=None):
+    """Full-size layer-batched launch (the library's split choice), sampled rows of `layers` against the
+    oracle.  q_scale multiplies the queries (a power of two: exact in bf16) to sharpen the softmax;
+    needle = (layer, row, head, slot) plants at that slot of the row's KV head a key equal to 4x the
+    query, so that row's output is that slot's value row."""
     c = synth.gqa_case(w, seed=seed, device="cuda")
     q, k, v = c["q_pre"], c["ctx_k"], c["ctx_v"]
-    out = torch.zeros(w.n_layers, w.n_q, w.n_heads, w.head_dim, dtype=torch.bfloat16, device="cuda")
-    log("full-size attention", w.name, "layers", layers, "rows", len(rows))
-    pkv.suffix_attention(q, k, v, out, c["q_pos"].cuda(), torch.tensor([w.kv_len], dtype=torch.int32,
-                         device="cuda"), w.scale, max_kv_len=w.kv_len)
-    torch.cuda.synchronize()
-    got = host_bits(out[layers][:, rows])
+    if q_scale != 1:
+        q.mul_(q_scale)
+    if needle is not None:
+        nl, nr, nh, slot = needle
+        k[nl, nh // (w.n_heads // w.n_kv_heads), slot] = (q[nl, nr, nh].float() * 4).to(k.dtype)
+    log("full-size attention", w.name, "layers", layers, "rows", len(rows), "q x%g" % q_scale, "needle", needle)
+    out, ws = guarded_attention(q, k, v, c["q_pos"].cuda(), torch.tensor([w.kv_len], dtype=torch.int32,
+                                device="cuda"), w.scale, w.kv_len, w.head_dim)
+    got = host_bits(out.t[layers][:, rows])
     qh, kh, vh = host_bits(q[layers]), host_bits(k[layers]), host_bits(v[layers])
     want, _ = oracle_attention(w, qh, kh, vh, c["q_pos"].numpy(), w.kv_len, rows=rows)
-    log("  ", check_attention_close(got, want))
+    log("  workspace %d B," % ws, check_attention_close(got, want), "output rms %.3g" % np.sqrt((want ** 2).mean()))
+    if needle is not None:
+        li, ri = layers.index(nl), list(rows).index(nr)
+        g = nh // (w.n_heads // w.n_kv_heads)
+        np.testing.assert_allclose(bits_to_f64(got[li, ri, nh]), bits_to_f64(vh[li, g, slot]), atol=3e-2)
 
 
 def test_full_gqa8b():
@@ -243,6 +255,21 @@ def test_full_gqa8b():
 def test_full_long32k_sampled():
     rows = np.unique(np.concatenate([[0, 1, 511, 1022, 1023], np.random.default_rng(0).integers(0, 1024, 11)]))
     full_gqa(synth.LONG32K, layers=[0, 27], rows=rows)
+
+
+def test_full_long32k_sharpened():
+    """Queries x4 over 50176 keys, split by the planner: sharp scores across every split, so the lazy
+    rescale of the running maximum and the split merge both matter."""
+    rows = np.unique(np.concatenate([[0, 700, 1023], np.random.default_rng(1).integers(0, 1024, 9)]))
+    full_gqa(synth.LONG32K, layers=[0, 27], rows=rows, q_scale=4)
+
+
+def test_full_long32k_needle():
+    """A planted key late in the cache (slot 40000, inside the last split) for row 700, head 9 of layer
+    27: the running maximum jumps far past the lazy threshold mid-stream and the row returns the
+    needle's value row; the other sampled rows of that KV head see the needle at random scores."""
+    rows = np.array([0, 1, 699, 700, 701, 1023])
+    full_gqa(synth.LONG32K, layers=[0, 27], rows=rows, needle=(27, 700, 9, 40000))
 
 
 # ---- MLA (absorbed form; Sec. 8 MLA adapter) ----------------------------------
@@ -316,23 +343,47 @@ def test_mla_splice_then_attend():
         check_attention_close(got[l], want)
 
 
-def test_full_mla_sampled():
+def full_mla(q_scale=1, needle=None, rows=np.array([0, 1, 63, 126, 127]), layers=(0, 26)):
+    """Full-size layer-batched MLA launch, sampled rows against the oracle (q_scale as in full_gqa).
+    needle = (layer, row, head, slot): the k_pe channels of that slot's latent row become 16x the
+    row's q_pe (exact in bf16), a score of about 16 * 64 * scale = 74 against N(0,1)-sized ones; its
+    512 latent channels, the value, stay N(0,1), so the row returns them."""
     w = synth.MLA
     c = synth.gqa_case(w, seed=0, device="cuda")
     q, k = c["q_pre"], c["ctx_k"]
-    out = torch.zeros(w.n_layers, w.n_q, w.n_heads, 512, dtype=torch.bfloat16, device="cuda")
-    log("full-size MLA attention")
-    pkv.suffix_attention(q, k, k[..., :512], out, c["q_pos"].cuda(),
-                         torch.tensor([w.kv_len], dtype=torch.int32, device="cuda"), w.scale, max_kv_len=w.kv_len,
-                         variant=pkv.PKV_ATTN_MLA)
-    torch.cuda.synchronize()
-    rows = np.array([0, 1, 63, 126, 127])
-    for layer in (0, 26):
+    if q_scale != 1:
+        q.mul_(q_scale)
+    if needle is not None:
+        nl, nr, nh, slot = needle
+        k[nl, 0, slot, 512:] = (q[nl, nr, nh, 512:].float() * 16).to(k.dtype)
+    log("full-size MLA attention", "q x%g" % q_scale, "needle", needle)
+    out, ws = guarded_attention(q, k, k[..., :512], c["q_pos"].cuda(),
+                                torch.tensor([w.kv_len], dtype=torch.int32, device="cuda"), w.scale, w.kv_len, 512,
+                                variant=pkv.PKV_ATTN_MLA)
+    for layer in layers:
         qh = host_bits(q[layer])[rows]
         kh = host_bits(k[layer])
         want, _ = oracle.attention(np.ascontiguousarray(qh), kh, kh[..., :512], c["q_pos"].numpy()[rows], w.kv_len,
                                    w.scale)
-        log("  layer", layer, check_attention_close(host_bits(out[layer])[rows], want))
+        got = host_bits(out.t[layer])[rows]
+        log("  layer", layer, "workspace %d B" % ws, check_attention_close(got, want))
+        if needle is not None and layer == needle[0]:
+            ri = list(rows).index(needle[1])
+            np.testing.assert_allclose(bits_to_f64(got[ri, needle[2]]), bits_to_f64(kh[0, needle[3], :512]),
+                                       atol=3e-2)
+
+
+def test_full_mla_sampled():
+    full_mla()
+
+
+def test_full_mla_sharpened():
+    full_mla(q_scale=4)
+
+
+def test_full_mla_needle():
+    """Slot 20000 (in the second of the planner's splits) of layer 26 is the needle for row 50, head 3."""
+    full_mla(needle=(26, 50, 3, 20000), rows=np.array([0, 49, 50, 51, 127]))
 
 
 @pytest.mark.parametrize("name", ["gqa8b", "long32k", "mla"])
@@ -345,19 +396,68 @@ def test_full_one_layer_per_launch_sampled(name):
     q, k = c["q_pre"], c["ctx_k"]
     v = k[..., : w.v_dim] if w.mla else c["ctx_v"]
     variant = pkv.PKV_ATTN_MLA if w.mla else pkv.PKV_ATTN_GQA
-    out = torch.zeros(w.n_layers, w.n_q, w.n_heads, w.v_dim, dtype=torch.bfloat16, device="cuda")
     kl = torch.tensor([w.kv_len], dtype=torch.int32, device="cuda")
     layers = (0, w.n_layers - 1)
     log("one layer per launch", name, "layers", layers)
-    for l in layers:
-        pkv.suffix_attention(q[l:l + 1], k[l:l + 1], v[l:l + 1], out[l:l + 1], c["q_pos"].cuda(), kl, w.scale,
-                             max_kv_len=w.kv_len, variant=variant)
-    torch.cuda.synchronize()
     rows = np.unique(np.array([0, 1, w.n_q // 2, w.n_q - 2, w.n_q - 1]))
     q_pos = c["q_pos"].numpy()
     for l in layers:
+        out, ws = guarded_attention(q[l:l + 1], k[l:l + 1], v[l:l + 1], c["q_pos"].cuda(), kl, w.scale, w.kv_len,
+                                    w.v_dim, variant=variant)
         qh = np.ascontiguousarray(host_bits(q[l])[rows])
         kh = host_bits(k[l])
         vh = kh[..., : w.v_dim] if w.mla else host_bits(v[l])
         want, _ = oracle.attention(qh, kh, vh, q_pos[rows], w.kv_len, w.scale)
-        log("  layer", l, check_attention_close(host_bits(out[l])[rows], want))
+        log("  layer", l, "workspace %d B" % ws, check_attention_close(host_bits(out.t[0])[rows], want))
+
+
+@pytest.mark.parametrize("variant,splits", [("gqa", 0), ("gqa", 1), ("gqa", 3), ("mla", 0), ("mla", 1),
+                                            ("fp32", 0), ("fp32", 1)])
+def test_rows_no_sequence_owns_are_untouched(variant, splits):
+    """cu_q[n_seqs] < total_q and one empty sequence: the rows after the last sequence are not written
+    (they keep the sentinel), with one pass and with split partials merged (the planner's choice splits
+    these few long rows), and the owned rows match the oracle."""
+    nqs, kvls = [7, 0, 12], [3000, 500, 2100]
+    spare = 5                                              # rows after cu_q[n_seqs]
+    L = 2
+    if variant == "mla":
+        H, Hkv, d, dv, dt = 16, 1, 576, 512, torch.bfloat16
+    else:
+        H, Hkv, d, dv = 8, 2, 128, 128
+        dt = torch.float32 if variant == "fp32" else torch.bfloat16
+    g = synth.Draws(21, "cpu")
+    caps = [kl + 3 for kl in kvls]
+    bases = np.concatenate([[0], np.cumsum(caps)[:-1]]).astype(np.int64)
+    k = g.normal((L, Hkv, int(sum(caps)), d), dtype=dt)
+    v = k[..., :dv] if variant == "mla" else g.normal((L, Hkv, int(sum(caps)), dv), dtype=dt)
+    total = sum(nqs) + spare
+    q = g.normal((L, total, H, d), dtype=dt)
+    q_pos = np.concatenate([np.arange(kl - n, kl) for n, kl in zip(nqs, kvls)] + [np.zeros(spare)]).astype(np.int32)
+    cu = np.concatenate([[0], np.cumsum(nqs)]).astype(np.int32)
+    kd, vd = k.cuda(), (None if variant == "mla" else v.cuda())
+    vd = kd[..., :dv] if variant == "mla" else vd
+    out, ws = guarded_attention(q.cuda(), kd, vd, torch.from_numpy(q_pos).cuda(),
+                                torch.tensor(kvls, dtype=torch.int32, device="cuda"), 1 / math.sqrt(d), max(kvls), dv,
+                                n_seqs=len(nqs), cu_q=torch.from_numpy(cu).cuda(),
+                                kv_base=torch.from_numpy(bases).cuda(), max_q=max(nqs), n_splits=splits,
+                                variant=pkv.PKV_ATTN_MLA if variant == "mla" else pkv.PKV_ATTN_GQA)
+    log("  %s splits=%d: workspace %d B" % (variant, splits, ws))
+    if splits == 0:
+        assert ws > 0, "the planner was expected to split these rows"
+    assert out.untouched((slice(None), slice(int(cu[-1]), total))), "rows after cu_q[n_seqs] were written"
+    qn = q.numpy() if dt == torch.float32 else host_bits(q)
+    kn = k.numpy() if dt == torch.float32 else host_bits(k)
+    vn = kn[..., :dv] if variant == "mla" else (v.numpy() if dt == torch.float32 else host_bits(v))
+    got = out.t.cpu().numpy() if dt == torch.float32 else host_bits(out.t)
+    for s_i in range(len(nqs)):
+        if nqs[s_i] == 0:
+            continue
+        rows = slice(cu[s_i], cu[s_i + 1])
+        ks = slice(bases[s_i], bases[s_i] + caps[s_i])
+        for l in range(L):
+            want, _ = oracle.attention(np.ascontiguousarray(qn[l, rows]), np.ascontiguousarray(kn[l][:, ks]),
+                                       np.ascontiguousarray(vn[l][:, ks]), q_pos[rows], kvls[s_i], 1 / math.sqrt(d))
+            if dt == torch.float32:
+                assert np.linalg.norm(got[l, rows] - want) / np.linalg.norm(want) <= 1e-5
+            else:
+                check_attention_close(got[l, rows], want)
