@@ -317,6 +317,31 @@ pkv_status pkv_suffix_attention_paged(const void* q, const void* k_pages, const 
                                       const pkv_attn_desc* desc, const pkv_paged_cache* paging,
                                       void* workspace, size_t workspace_bytes, void* stream);
 
+/* Bytes of the static device scratch behind pkv_suffix_attention_noalloc. */
+#define PKV_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* Allocation-free suffix attention, for callers that cannot allocate device
+ * memory or pass a workspace: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Same arguments, semantics and
+ * errors as pkv_suffix_attention without workspace / workspace_bytes.  The
+ * split-KV partials go to a static device array of PKV_NOALLOC_SCRATCH_BYTES
+ * that the library holds on every GPU it has run this call on, until the
+ * process ends; the call allocates and frees nothing and records no memset.
+ * Size limit: with desc->n_splits = 0 the split count is the library's choice,
+ * lowered if needed until the partials fit the scratch (1 split needs none);
+ * an explicit desc->n_splits whose partials exceed the scratch is rejected
+ * with PKV_ERR_SHAPE.  Every call on one GPU shares that GPU's scratch: calls
+ * that overlap in time on one GPU (different streams, or host threads without
+ * ordering) race and give undefined results; calls ordered on one stream are
+ * safe.  Nothing in the scratch needs clearing between calls (each call
+ * writes every partial it reads).  The first call on a device looks up the
+ * scratch's address there (hipGetSymbolAddress); a failure of that lookup is
+ * PKV_ERR_DEVICE. */
+pkv_status pkv_suffix_attention_noalloc(const void* q, const void* k_cache, const void* v_cache, void* out,
+                                        const int32_t* q_pos, const int32_t* kv_len, int32_t n_q_heads,
+                                        int32_t n_kv_heads, int32_t head_dim, float scale,
+                                        const pkv_attn_desc* desc, void* stream);
+
 /* ---------------------------------------------------------------------------
  * Diagnostics
  * ------------------------------------------------------------------------- */

@@ -6,10 +6,19 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "pkv.h"
 #include "pkv_internal.h"
 
 #define PKV_EXPORT extern "C" __attribute__((visibility("default")))
+
+// Split-KV scratch of pkv_suffix_attention_noalloc: a file-scope device array,
+// so that entry point never allocates.  Each GPU the library runs on holds its
+// own copy (PKV_NOALLOC_SCRATCH_BYTES) until the process ends.  In host code
+// `scratch` names a host-side stand-in, not device memory: kernels only ever
+// get the per-device address that hipGetSymbolAddress returns for it.
+static __device__ __align__(256) unsigned char scratch[PKV_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -403,6 +412,39 @@ PKV_EXPORT size_t pkv_attention_workspace_size(const pkv_attn_desc* desc, int32_
 
 namespace {
 
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};   // device address of `scratch`, per device
+
+// Device address of `scratch` on the current device, looked up once per device
+// (with that device current: each GPU holds the array at its own address).
+pkv_status scratch_on_current_device(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(PKV_ERR_DEVICE, "hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(PKV_ERR_UNSUPPORTED, "device %d: the allocation-free entry point serves devices 0..%d", dev,
+                    kMaxDevices - 1);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(PKV_ERR_DEVICE, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+        g_scratch_dev[dev] = p;
+    }
+    *out = g_scratch_dev[dev];
+    return PKV_OK;
+}
+
+// Workspace layout shared by both attention entry points:
+// [split][layer][row][head][d_v] partial outputs, then [split][layer][row][head] LSEs.
+void set_workspace(pkv::AttnArgs& a, void* workspace) {
+    const size_t rows = (size_t)a.n_splits * a.n_layers * a.total_q * a.n_heads;
+    a.ws_o = (float*)workspace;
+    a.ws_lse = a.ws_o + rows * a.head_dim_v;
+}
+
 pkv_status run_attention(const void* q, const void* k_cache, const void* v_cache, void* out, const int32_t* q_pos,
                          const int32_t* kv_len, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, float scale,
                          const pkv_attn_desc* desc, const pkv_paged_cache* paging, void* workspace,
@@ -420,12 +462,7 @@ pkv_status run_attention(const void* q, const void* k_cache, const void* v_cache
         if (!aligned16(workspace)) return fail(PKV_ERR_ALIGN, "workspace must be 16-byte aligned");
     }
     a.n_splits = splits;
-    if (need > 0) {
-        // [split][layer][row][head][d_v] partial outputs, then [split][layer][row][head] LSEs
-        const size_t rows = (size_t)splits * a.n_layers * a.total_q * a.n_heads;
-        a.ws_o = (float*)workspace;
-        a.ws_lse = a.ws_o + rows * a.head_dim_v;
-    }
+    if (need > 0) set_workspace(a, workspace);
     if (a.total_q == 0) return ok();
     return device_status(pkv::launch_attention(a, (hipStream_t)stream), "suffix_attention launch");
 }
@@ -450,6 +487,37 @@ PKV_EXPORT pkv_status pkv_suffix_attention_paged(const void* q, const void* k_pa
     if (!paging) return fail(PKV_ERR_NULL, "paging is NULL");
     return run_attention(q, k_pages, v_pages, out, q_pos, kv_len, n_q_heads, n_kv_heads, head_dim, scale, desc,
                          paging, workspace, workspace_bytes, stream);
+}
+
+PKV_EXPORT pkv_status pkv_suffix_attention_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                                                   void* out, const int32_t* q_pos, const int32_t* kv_len,
+                                                   int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                                   float scale, const pkv_attn_desc* desc, void* stream) {
+    pkv::AttnArgs a;
+    pkv_status st = check_attention(q, k_cache, v_cache, out, q_pos, kv_len, n_q_heads, n_kv_heads, head_dim,
+                                    scale, desc, true, a);
+    if (st != PKV_OK) return st;
+    int splits = pkv::attention_splits(a);
+    size_t need = pkv::attention_workspace_bytes(a, splits);
+    if (need > PKV_NOALLOC_SCRATCH_BYTES) {
+        if (desc->n_splits > 0)
+            return fail(PKV_ERR_SHAPE,
+                        "%d splits need %zu bytes of partials, more than the %zu-byte scratch of the "
+                        "allocation-free entry point (use fewer splits, n_splits = 0, or pkv_suffix_attention "
+                        "with a workspace)",
+                        splits, need, (size_t)PKV_NOALLOC_SCRATCH_BYTES);
+        while (splits > 1 && pkv::attention_workspace_bytes(a, splits) > PKV_NOALLOC_SCRATCH_BYTES) --splits;
+        need = pkv::attention_workspace_bytes(a, splits);
+    }
+    a.n_splits = splits;
+    if (need > 0) {
+        void* sp = nullptr;
+        st = scratch_on_current_device(&sp);
+        if (st != PKV_OK) return st;
+        set_workspace(a, sp);
+    }
+    if (a.total_q == 0) return ok();
+    return device_status(pkv::launch_attention(a, (hipStream_t)stream), "suffix_attention_noalloc launch");
 }
 
 PKV_EXPORT const char* pkv_last_error(void) { return g_err; }

@@ -75,7 +75,8 @@ class pkv_paged_cache(ctypes.Structure):
 
 SYMBOLS = ("pkv_reposition_splice", "pkv_reposition_splice_freqs", "pkv_reposition_splice_paged",
            "pkv_reposition_splice_batched", "pkv_attention_workspace_size", "pkv_suffix_attention",
-           "pkv_suffix_attention_paged", "pkv_last_error", "pkv_version")
+           "pkv_suffix_attention_paged", "pkv_suffix_attention_noalloc", "pkv_last_error", "pkv_version")
+PKV_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 _lib = None
 
@@ -118,6 +119,9 @@ def lib() -> ctypes.CDLL:
     L.pkv_suffix_attention_paged.argtypes = [P, P, P, P, P, P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                              ctypes.c_float, ctypes.POINTER(pkv_attn_desc),
                                              ctypes.POINTER(pkv_paged_cache), P, ctypes.c_size_t, P]
+    L.pkv_suffix_attention_noalloc.restype = ctypes.c_int
+    L.pkv_suffix_attention_noalloc.argtypes = [P, P, P, P, P, P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                               ctypes.c_float, ctypes.POINTER(pkv_attn_desc), P]
     L.pkv_last_error.restype = ctypes.c_char_p
     L.pkv_last_error.argtypes = []
     L.pkv_version.restype = ctypes.c_int32
@@ -212,6 +216,14 @@ def pkv_suffix_attention_paged(q, k_pages, v_pages, out, q_pos, kv_len, n_q_head
         _ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(out), _ptr(q_pos), _ptr(kv_len), int(n_q_heads),
         int(n_kv_heads), int(head_dim), float(scale), ctypes.byref(desc) if desc is not None else None,
         ctypes.byref(paging) if paging is not None else None, _ptr(workspace), int(workspace_bytes),
+        _stream(stream))
+
+
+def pkv_suffix_attention_noalloc(q, k_cache, v_cache, out, q_pos, kv_len, n_q_heads, n_kv_heads, head_dim, scale,
+                                 desc, stream=None) -> int:
+    return lib().pkv_suffix_attention_noalloc(
+        _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(out), _ptr(q_pos), _ptr(kv_len), int(n_q_heads),
+        int(n_kv_heads), int(head_dim), float(scale), ctypes.byref(desc) if desc is not None else None,
         _stream(stream))
 
 
