@@ -36,10 +36,10 @@ def compile_flags():
     ]
 
 
-# Per-source device-compiler options.  The MLA kernel keeps its 128 output
-# accumulators in VGPRs: left to its heuristics the compiler parks them in
-# AGPRs and copies all of them to VGPRs and back on every key tile for the
-# (rarely taken) rescale, which costs about 13% of the kernel's time.
+# Per-source device-compiler options.  The MLA kernel's score MFMAs
+# accumulate in VGPRs (its output accumulators, written only by inline
+# assembly, take the whole AGPR file): the compiler chooses one register file
+# for all MFMA builtins of a function.
 FILE_FLAGS = {
     "attn_mla_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }

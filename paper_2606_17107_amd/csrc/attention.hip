@@ -11,6 +11,8 @@ hipError_t launch_attn_mla_bf16(const AttnArgs& a, const Plan& p, dim3 grid, hip
 
 namespace {
 
+constexpr int kCUs = 256;   // compute units of an MI355X
+
 // fp32 GQA kernel: four lanes per row, each holding D/4 channels of q and o;
 // K/V tiles of 32 keys staged in LDS; fp32 online softmax, one step per tile.
 template <int D>
@@ -200,38 +202,42 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
     if (qi >= nq) return;
     const int64_t row = q0 + qi;
     const int64_t item = ((int64_t)layer * a.total_q + row) * a.n_heads + head;
-    // Loads go out CB splits at a time (independent, so their latencies
-    // overlap); the sums still run over s = 0, 1, ... in order.
-    constexpr int CB = 8;
+    // The log-sum-exps and partial outputs of up to CB splits are loaded in
+    // one batch (independent loads: one memory round trip), then weighted by
+    // w_s = 2^(lse_s - max) and summed in split order; a later batch (more
+    // than CB splits) rescales the sums to its larger maximum.
+    constexpr int CB = 16;
     const int ns = a.n_splits;
-    float mx = -INFINITY;
+    float mx = -INFINITY, wsum = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int s0 = 0; s0 < ns; s0 += CB) {
         float l[CB];
+        f32x4 v[CB];
 #pragma unroll
-        for (int j = 0; j < CB; ++j) l[j] = s0 + j < ns ? a.ws_lse[(int64_t)(s0 + j) * items + item] : -INFINITY;
+        for (int j = 0; j < CB; ++j) {
+            const bool in = s0 + j < ns;
+            l[j] = in ? a.ws_lse[(int64_t)(s0 + j) * items + item] : -INFINITY;
+            v[j] = in ? *(const f32x4*)(a.ws_o + ((int64_t)(s0 + j) * items + item) * dv + c * 4)
+                      : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        float bm = -INFINITY;
 #pragma unroll
-        for (int j = 0; j < CB; ++j) mx = fmaxf(mx, l[j]);
-    }
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    float wsum = 0.f;
-    if (mx != -INFINITY) {
-        for (int s0 = 0; s0 < ns; s0 += CB) {
-            float l[CB];
-            f32x4 v[CB];
-#pragma unroll
-            for (int j = 0; j < CB; ++j) {
-                const bool in = s0 + j < ns;
-                l[j] = in ? a.ws_lse[(int64_t)(s0 + j) * items + item] : -INFINITY;
-                v[j] = in ? *(const f32x4*)(a.ws_o + ((int64_t)(s0 + j) * items + item) * dv + c * 4)
-                          : f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < CB; ++j) bm = fmaxf(bm, l[j]);
+        if (bm == -INFINITY) continue;
+        if (bm > mx) {
+            if (mx != -INFINITY) {
+                const float r = __builtin_amdgcn_exp2f(mx - bm);
+                acc *= r;
+                wsum *= r;
             }
+            mx = bm;
+        }
 #pragma unroll
-            for (int j = 0; j < CB; ++j) {
-                if (l[j] == -INFINITY) continue;
-                const float w = __builtin_amdgcn_exp2f(l[j] - mx);
-                acc += w * v[j];
-                wsum += w;
-            }
+        for (int j = 0; j < CB; ++j) {
+            if (l[j] == -INFINITY) continue;
+            const float w = __builtin_amdgcn_exp2f(l[j] - mx);
+            acc += w * v[j];
+            wsum += w;
         }
     }
     const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
@@ -254,8 +260,7 @@ Plan make_plan(const AttnArgs& a, int splits) {
     const int64_t m_rows = (int64_t)a.max_q * p.G;
     int tile = 32;
     if (a.variant == 1) {
-        // MLA: two wave pairs, each sharing 32 rows (two score-channel halves
-        // and two output halves); 32-key tiles in 2 LDS stages.
+        // MLA: four waves of 32 whole rows; 32-key tiles in 2 LDS stages.
         p.qb = 1;
         p.nw = 4;
         p.ns = 2;
@@ -267,7 +272,7 @@ Plan make_plan(const AttnArgs& a, int splits) {
         p.nw = 4;
         p.ns = 4;
     }
-    p.BM = a.dtype == 1 ? 64 : (a.variant == 1 ? p.nw / 2 * 32 : p.nw * 32 * p.qb);
+    p.BM = a.dtype == 1 ? 64 : p.nw * 32 * p.qb;
     p.rbs = (int)((m_rows + p.BM - 1) / p.BM);
     if (p.rbs < 1) p.rbs = 1;
     p.splits = splits;
@@ -280,7 +285,7 @@ Plan make_plan(const AttnArgs& a, int splits) {
 
 // Workgroups that fit on one CU at once (LDS and register bound).
 int wgs_per_cu(const AttnArgs& a, const Plan& p) {
-    if (a.variant == 1) return 1;                     // MLA: 36 KB stages plus the score exchange
+    if (a.variant == 1) return 1;                     // MLA: two 36 KB stages, one wave per SIMD
     const int tile = 32;                              // keys per K/V tile
     const int lds = p.ns * 2 * tile * a.head_dim * 2;
     const int n = (160 * 1024) / lds;
@@ -305,20 +310,20 @@ int attention_splits(const AttnArgs& a) {
     // fixed cost is about 20 us, the combine streams at about 5 TB/s.  At
     // least 512 keys per split, at most 32 splits.
     const Plan p = make_plan(a, 1);
-    const int64_t wgs = (int64_t)p.n_groups * p.rbs;
+    const int64_t wgs = (int64_t)p.n_groups * p.rbs;   // workgroups per split
     if (a.dtype == 1) {
         // fp32 path (small problems): one workgroup per CU, at least 64 keys
         // per split, at most 32 splits.
-        int64_t s = (256 + wgs - 1) / wgs;
+        int64_t s = (kCUs + wgs - 1) / wgs;
         const int64_t max_s = a.max_kv_len / 64;
         if (s > max_s) s = max_s;
         if (s > 32) s = 32;
         return s < 1 ? 1 : (int)s;
     }
-    const int64_t slots = 256 * (int64_t)wgs_per_cu(a, p);
+    const int64_t slots = kCUs * (int64_t)wgs_per_cu(a, p);
     const double rate = a.variant == 1 ? 0.75e15 : 1.0e15;
-    const double wg_flops = (double)p.BM * a.max_kv_len * (a.head_dim + a.head_dim_v) * 2.0;
     const double slot_rate = rate / (double)slots;
+    const double wg_flops = (double)p.BM * a.max_kv_len * (a.head_dim + a.head_dim_v) * 2.0;
     const double comb_bytes = (double)a.n_layers * a.total_q * a.n_heads * (a.head_dim_v + 1) * 4.0 * 2.0;
     int best = 1;
     double best_t = 1e30;

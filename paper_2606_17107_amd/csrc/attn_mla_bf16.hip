@@ -1,36 +1,45 @@
 // bf16 MLA suffix attention (absorbed form) for gfx950.
 //
 // The MLA cache keeps, per token, one latent row [c_kv (512) | k_pe (64)]
-// shared by every head (paper Sec. 8, MLA adapter: a position-free latent
-// plus a small decoupled-RoPE sub-vector).  With absorbed queries
-// q = [q_latent (512) | q_pe (64)] per head, the scores run over all 576
-// channels and the values are the 512 latent channels of the same row:
+// shared by every head (paper Sec. 8, MLA adapter: the latent is position-free
+// and only the small decoupled-RoPE slice carries positions).  With absorbed
+// queries q = [q_latent (512) | q_pe (64)] per head, the scores run over all
+// 576 channels and the values are the 512 latent channels of the same row:
 //     o_h = sum_j softmax_j(scale <q_h, row_j>) row_j[0:512]
 //
 // Work decomposition (one KV "head", so every query head is a row):
-//   * MFMA 32x32x16 bf16 -> fp32; row m <-> query m / H, head m % H.  Two
-//     waves share each block of 32 rows.  Each forms the partial scores over
-//     one half of the 576 channels (its Q^T half, 72 VGPRs, in registers),
-//     the two partials are exchanged through LDS and added (fp32), both waves
-//     run the same online softmax, and each accumulates one 256-channel half
-//     of O^T (128 values per lane).
-//   * S^T = K Q^T (36 k-steps), online softmax in-lane as in the GQA kernel,
-//     O^T += V^T P^T where V^T comes from the same LDS tile through
-//     ds_read_b64_tr_b16 (channels 0..511).
-//   * Tiles of 32 keys (36 KB) stream HBM -> LDS by LDS-DMA through NS
-//     stages; chunks XOR-swizzled by the key as in the GQA kernel.
-//   * Four waves (two pairs, 64 rows) per workgroup and two LDS stages
-//     (eight waves, two per SIMD, and three stages were measured no faster).
-//   * One wave per SIMD, so every stall is exposed: the operand reads of each
-//     MFMA chain are issued in fenced groups a fixed distance ahead (the
-//     compiler's own order left each MFMA waiting on its read), the second
-//     half of the probabilities is formed between the PV MFMAs that consume
-//     the first, and the row maximum crosses the two wave halves with a
-//     permlane swap.  The 128 output accumulators live in VGPRs (a per-file
-//     compiler option): left in AGPRs, every tile copied them out and back
-//     for the rarely taken rescale.
-//   * Rows wholly owned by one wave (all 576 score and 512 value channels, no
-//     exchange) would need 144 + 256 registers for Q^T and O and do not fit.
+//   * MFMA 32x32x16 bf16 -> fp32; row m <-> query m / H, head m % H.  Each
+//     wave owns 32 rows outright: their Q^T over all 576 channels (36 k-step
+//     operands, 144 VGPRs) and their O^T over all 512 value channels (16
+//     blocks, 256 accumulators in the AGPR file).  Four waves share every K/V
+//     tile in LDS, so one workgroup covers 128 rows and a tile byte serves all
+//     of them.
+//   * S^T = K Q^T (36 MFMAs, one accumulation chain), online softmax in-lane
+//     (a lane holds 16 keys of one row; the two halves of a row pair up with
+//     a permlane swap), O^T += V^T P^T (32 MFMAs) where V^T comes from the
+//     same LDS tile through ds_read_b64_tr_b16 (channels 0..511).  Every MFMA
+//     reads one 1 KB operand from LDS; the LDS-DMA fill adds 36 KB per tile
+//     for the workgroup, about 1.13 KB of LDS traffic per MFMA in all.
+//   * Tiles of 32 keys (36 KB) stream HBM -> LDS by LDS-DMA through 2 stages
+//     (one tile in flight while one is consumed); 16-byte chunks are
+//     XOR-swizzled by key against bank conflicts.
+//   * One wave per SIMD: the 256 output accumulators fill the AGPR file and
+//     Q^T with the working set fills the VGPRs.  The compiler chooses one
+//     register file for all MFMA accumulators of a function, so the score
+//     MFMAs are builtins accumulating in VGPRs (a per-file compiler option)
+//     and the PV MFMAs are inline assembly accumulating in AGPRs ("+a"
+//     operands); nothing else touches the accumulators until the epilogue,
+//     which first waits out the MFMA write latency.  The wave hides its own
+//     latencies: the LDS operand reads of each MFMA chain are issued in fenced
+//     groups a fixed distance ahead, and the second half of the
+//     probabilities is formed between the PV MFMAs that consume the first.
+//   * The accumulators are never rescaled.  Each row's reference maximum is
+//     the maximum of its first tile with a visible key; later probabilities
+//     2^(s - ref) may exceed 1, which costs no relative precision in fp32 and
+//     bf16, up to 2^32.  A tile whose maximum exceeds the reference by more
+//     than that (a score spike far above everything before it) marks the
+//     workgroup, which then runs its key range a second time with every
+//     row's exact maximum, known from the first pass, as the reference.
 #include <type_traits>
 
 #include "attn_common.h"
@@ -38,7 +47,7 @@
 namespace pkv {
 namespace {
 
-constexpr int kMlaWaves = 4;    // two wave pairs, 64 rows
+constexpr int kMlaWaves = 4;    // 32 rows per wave, 128 per workgroup
 constexpr int kMlaStages = 2;   // LDS stages of 32-key tiles
 constexpr int kMlaAhead = 2;    // LDS operand reads issued this many operands ahead of their MFMA
 
@@ -61,19 +70,17 @@ template <bool PAGED>
 __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnArgs a, Plan p) {
     constexpr int NS = kMlaStages, NW = kMlaWaves;
     constexpr int NBLK = MBN * MCH / 64;       // 64-lane LDS-DMA blocks per tile: 36
-    constexpr int PER = (NBLK + NW - 1) / NW;  // blocks of the busiest wave per tile
-    constexpr int KS = DQK / 16 / 2;           // k-steps per wave (its half of the channels): 18
-    constexpr int DB = DV / 64;                // 32-channel blocks per wave (its half of DV): 8
-    constexpr int RPW = NW / 2 * 32;           // rows per workgroup
+    constexpr int PER = NBLK / NW;             // blocks per wave per tile: 9
+    constexpr int KS = DQK / 16;               // k-steps over the score channels: 36
+    constexpr int DB = DV / 32;                // 32-channel output blocks: 16
+    constexpr int RPW = NW * 32;               // rows per workgroup
     constexpr int TE = MBN * DQK;              // elements per tile
-    static_assert(NW % 2 == 0, "pairs of waves share 32 rows");
-    static_assert(NS == 2, "two LDS stages");
+    static_assert(NBLK % NW == 0, "tile loads must split evenly over the waves");
+    static_assert(NS >= 2 && NS <= 4 && (NS - 2) * PER < 64, "2..4 stages within the vmcnt range");
 
-    __shared__ __attribute__((aligned(16))) uint16_t t0_[TE], t1_[TE];
+    __shared__ __attribute__((aligned(16))) uint16_t stage_lds[NS * TE];
     __shared__ int red[NW], red_start[NW];
-    // Partial-score exchange: [wave][4 chunks][64 lanes] x 16 bytes.
-    __shared__ __attribute__((aligned(16))) float xch[NW * 4 * 64 * 4];
-    auto stage = [&](int st) -> uint16_t* { return st == 0 ? t0_ : t1_; };
+    auto stage = [&](int st) __attribute__((always_inline)) -> uint16_t* { return stage_lds + st * TE; };
 
     int group, rb;
     if (!decode(p, group, rb)) return;
@@ -85,7 +92,6 @@ __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnAr
     const int H = a.n_heads;
     const int M = si.nq * H;
     const int m0 = rb * RPW;
-    const int vhalf = (threadIdx.x >> 6) & 1;   // which 256-channel half of O this wave owns
     if (m0 >= M) return;
 
     const int tid = threadIdx.x;
@@ -94,7 +100,7 @@ __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnAr
     const int j = lane & 31;
     const int hl = lane >> 5;
 
-    const int m = m0 + (wave >> 1) * 32 + j;
+    const int m = m0 + wave * 32 + j;
     const bool row_ok = m < M;
     const int qi = row_ok ? m / H : 0;
     const int head = row_ok ? m - qi * H : 0;
@@ -107,7 +113,7 @@ __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnAr
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             u32x4 v = {0u, 0u, 0u, 0u};
-            if (row_ok) v = *(const u32x4*)(qrow + (vhalf * KS + ks) * 16 + hl * 8);
+            if (row_ok) v = *(const u32x4*)(qrow + ks * 16 + hl * 8);
             qf[ks] = __builtin_bit_cast(bf16x8, v);
         }
     }
@@ -141,16 +147,14 @@ __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnAr
     const uint16_t* kbase = (const uint16_t*)a.k + (int64_t)layer * a.k_stride[0] + si.base * a.k_stride[2];
     const int64_t kss = a.k_stride[2];
     const int last_key = loop_end - 1;
-    // Wave w moves blocks w, w + NW, ... of each tile (NBLK / NW or one more):
-    // lane l of block b fills LDS chunk slot 64b + l (key slot / 72, physical
-    // chunk slot % 72, holding logical chunk phys ^ mswz(key)).
-    const int n_mine = (NBLK - wave + NW - 1) / NW;   // wave-uniform
+    // Wave w moves blocks w, w + NW, ... of each tile: lane l of block b fills
+    // LDS chunk slot 64b + l (key slot / 72, physical chunk slot % 72, holding
+    // logical chunk phys ^ mswz(key)).
     int32_t src_off[PER];
     int key_of[PER];
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-        const int b = i < n_mine ? wave + i * NW : wave;   // idle slots mirror block `wave` (never issued)
-        const int slot = b * 64 + lane;
+        const int slot = (wave + i * NW) * 64 + lane;
         key_of[i] = slot / MCH;
         const int logical = (slot % MCH) ^ mswz(key_of[i]);
         src_off[i] = (int32_t)((int64_t)key_of[i] * kss * 2 + logical * 16);
@@ -158,7 +162,7 @@ __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnAr
     // Paged cache: a 32-key tile lies in one page (page sizes are multiples of 32).
     PageWindow pw;
     if constexpr (PAGED) pw.init(a.block_table, a, seq, k_begin >> a.page_shift);
-    auto issue = [&](int t0, uint16_t* dst_stage) {
+    auto issue = [&](int t0, uint16_t* dst_stage) __attribute__((always_inline)) {
         const char* kt;
         if constexpr (PAGED)
             kt = (const char*)(kbase + pw.offset(a, t0, a.k_page_stride, kss));
@@ -167,37 +171,35 @@ __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnAr
         const uint32_t lds0 = lds_addr_of(dst_stage + wave * 64 * 8);
         if (t0 + MBN <= loop_end) {   // full tile: no per-lane adjustment
 #pragma unroll
-            for (int i = 0; i < PER; ++i)
-                if (i < n_mine) lds_dma16(lds0 + i * NW * 1024, kt, (uint32_t)src_off[i]);
+            for (int i = 0; i < PER; ++i) lds_dma16(lds0 + i * NW * 1024, kt, (uint32_t)src_off[i]);
         } else {
+            // A tile that runs past the last visible key re-reads that key for
+            // the missing rows (masked later).
 #pragma unroll
             for (int i = 0; i < PER; ++i) {
-                if (i < n_mine) {
-                    const int over = t0 + key_of[i] - last_key;
-                    const uint32_t back = over > 0 ? (uint32_t)(over * (int32_t)(kss * 2)) : 0u;
-                    lds_dma16(lds0 + i * NW * 1024, kt, (uint32_t)src_off[i] - back);
-                }
+                const int over = t0 + key_of[i] - last_key;
+                const uint32_t back = over > 0 ? (uint32_t)(over * (int32_t)(kss * 2)) : 0u;
+                lds_dma16(lds0 + i * NW * 1024, kt, (uint32_t)src_off[i] - back);
             }
         }
     };
 
     // Per-lane LDS element offsets of the MFMA operands within a stage.  The
     // swizzle only permutes the low three bits of a chunk index, so:
-    //   K (A of S^T = K Q^T), k-step ks: logical chunk c0 + 2ks of key j
-    //     (c0 = 36 vhalf + hl) sits at kofs[ks & 3] + (ks >> 2) * 64;
+    //   K (A of S^T = K Q^T), k-step ks: logical chunk 2ks + hl of key j sits
+    //     at kofs[ks & 3] + (ks >> 2) * 64;
     //   V^T (A of O^T = V^T P^T), 16-key step st, half b, channel block db:
-    //     lane group g = lane >> 4 reads channels 256 vhalf + 32db + 16(g&1) +
-    //     4(sl&3)..+3 of key 16st + 8b + 4(g>>1) + (sl>>2), sl = lane & 15 (the
-    //     key order of the P^T accumulator); the swizzle of that key depends
-    //     only on its low four bits, so the read is at
-    //     vofs[db & 1][b] + 16st * 576 + (db >> 1) * 64.
+    //     lane group g = lane >> 4 reads channels 32db + 16(g&1) + 4(sl&3)..+3
+    //     of key 16st + 8b + 4(g>>1) + (sl>>2), sl = lane & 15 (the key order
+    //     of the P^T accumulator); the swizzle of that key depends only on its
+    //     low four bits, so the read is at vofs[db & 1][b] + 16st * 576 +
+    //     (db >> 1) * 64.
     int kofs[4], vofs[2][2];
     {
         const int sk = mswz(j);
-        const int c0 = vhalf * KS * 2 + hl;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const int c = c0 + 2 * q;
+            const int c = hl + 2 * q;
             kofs[q] = j * DQK + ((c & ~7) | ((c & 7) ^ sk)) * 8;
         }
         const int g = lane >> 4, sl = lane & 15;
@@ -208,22 +210,31 @@ __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnAr
             for (int b = 0; b < 2; ++b) {
                 const int key = b * 8 + vkey;
                 const int c7 = par * 4 + (g & 1) * 2 + ((sl & 3) >> 1);
-                vofs[par][b] = key * DQK + (vhalf * 32 + (c7 ^ mswz(key))) * 8 + (sl & 1) * 4;
+                vofs[par][b] = key * DQK + (c7 ^ mswz(key)) * 8 + (sl & 1) * 4;
             }
     }
 
+    // O^T accumulators, zeroed by an MFMA of zero operands (an assignment
+    // would let the compiler keep them in VGPRs).  The zero operand is often
+    // written by VALU just before: two wait states before the MFMA reads it.
     f32x16 o[DB];
+    const bf16x8 zero8 = {};
+    auto zero_o = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int db = 0; db < DB; ++db) o[db] = f32x16{};
-    float m_run = -INFINITY, l_run = 0.f;
+        for (int db = 0; db < DB; ++db)
+            asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %1, 0" : "=a"(o[db]) : "v"(zero8));
+    };
+    zero_o();
+    float m_run = -INFINITY;   // reference maximum (log2 units, scaled), fixed once set
+    float m_seen = -INFINITY;  // largest scaled score seen
+    float l_run = 0.f;
+    bool spike = false;        // some score exceeded the reference by more than kSpan
     const float sc2 = a.scale * kLog2e;
-    constexpr float kLazy = 8.0f;
+    constexpr float kSpan = 32.0f;
 
-    auto compute = [&](int t0, const uint16_t* ts, auto mask_tag) {
+    auto compute = [&](int t0, const uint16_t* ts, auto mask_tag) __attribute__((always_inline)) {
         constexpr bool MASK = decltype(mask_tag)::value;
-        // Partial S^T = K Q^T over this wave's 288 channels, 32 keys (one
-        // accumulation chain: dependent MFMAs on the same accumulator issue
-        // back to back).
+        // S^T = K Q^T over the 576 channels, 32 keys: one accumulation chain.
         // Fenced groups: MFMA ks, then the read of the operand A steps ahead,
         // so A LDS round trips stay in flight across the chain.
         constexpr int A = kMlaAhead < KS ? kMlaAhead : KS;
@@ -240,23 +251,6 @@ __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnAr
             s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[ks], qf[ks], s, 0, 0, 0);
             if (ks + A < KS) kop[ks + A] = k_operand(ks + A);
             __builtin_amdgcn_sched_barrier(0);
-        }
-        // Exchange the partial scores with the other wave of the pair (the
-        // lanes of both waves hold the same (key, row) elements).
-        float* mine = xch + wave * 1024;
-        const float* other = xch + (wave ^ 1) * 1024;
-#pragma unroll
-        for (int c = 0; c < 4; ++c)
-            *(f32x4*)(mine + (c * 64 + lane) * 4) = f32x4{s[4 * c], s[4 * c + 1], s[4 * c + 2], s[4 * c + 3]};
-        __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
-        bare_barrier();
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const f32x4 x = *(const f32x4*)(other + (c * 64 + lane) * 4);
-            s[4 * c] += x[0];
-            s[4 * c + 1] += x[1];
-            s[4 * c + 2] += x[2];
-            s[4 * c + 3] += x[3];
         }
         if (MASK) {
 #pragma unroll
@@ -281,16 +275,12 @@ __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnAr
             const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
             mx = fminf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
         }
-        const float msc = mx * sc2;
-        const bool up = msc > m_run + kLazy;
-        if (__builtin_amdgcn_ballot_w64(up) != 0) {
-            const float m_new = up ? msc : m_run;
-            const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
-            l_run *= alpha;
-#pragma unroll
-            for (int db = 0; db < DB; ++db) o[db] *= alpha;
-            m_run = m_new;
-        }
+        const float msc = mx * sc2;   // this tile's maximum of the scaled scores
+        m_seen = fmaxf(m_seen, msc);
+        // The row's first tile with a visible key sets the reference (a tile
+        // with none has msc = -inf, or NaN when the scale is 0).
+        if (m_run == -INFINITY && msc > -INFINITY) m_run = msc;
+        spike |= msc > m_run + kSpan;
         const float neg_m = m_run == -INFINITY ? 0.f : -m_run;
         float lsum = 0.f;
         auto prob = [&](int r) __attribute__((always_inline)) {
@@ -318,7 +308,6 @@ __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnAr
         // q = (16-key step q / DB, channel block q % DB), read A steps ahead.
         constexpr int NQ = 2 * DB;
         constexpr int AV = kMlaAhead < NQ ? kMlaAhead : NQ;
-        static_assert(DB == 8, "one second-half probability per first-half MFMA");
         auto v_operand = [&](int q) __attribute__((always_inline)) {
             const int st = q / DB, db = q % DB;
             s16x4 part[2];
@@ -336,7 +325,14 @@ __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnAr
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
-            o[q % DB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[q], pb[q / DB], o[q % DB], 0, 0, 0);
+            // The first MFMA reads pb[0], written by VALU just before: two
+            // wait states (the compiler does not see into the statement).
+            if (q == 0)
+                asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0"
+                             : "+a"(o[q % DB]) : "v"(vop[q]), "v"(pb[q / DB]));
+            else
+                asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0"
+                             : "+a"(o[q % DB]) : "v"(vop[q]), "v"(pb[q / DB]));
             if (q < 8) prob(8 + q);
             if (q == 7) pb[1] = pack(1);
             if (q + AV < NQ) vop[q + AV] = v_operand(q + AV);
@@ -345,43 +341,66 @@ __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnAr
         l_run += lsum;
     };
 
-    // Each wave waits for its own loads: n_mine per tile (PER or PER - 1).
-    auto wait_tiles = [&](int tiles_after, auto per_tag) {
-        constexpr int Q = decltype(per_tag)::value;
-        if (NS > 3 && tiles_after >= 3) wait_vmcnt<(NS > 3 ? 3 : 1) * Q>();
-        else if (NS > 2 && tiles_after >= 2) wait_vmcnt<(NS > 2 ? 2 : 1) * Q>();
-        else if (tiles_after == 1) wait_vmcnt<Q>();
-        else wait_vmcnt<0>();
+    // Stage i % NS holds tile i.  Each iteration waits for tile i (at most
+    // NS-2 later tiles stay in flight), then, after the barrier (every wave
+    // has finished tile i-1), refills tile i-1's stage with tile i+NS-1.
+    auto wait_outstanding = [&](int tiles_after) __attribute__((always_inline)) {
+        if (tiles_after >= NS - 2) {
+            wait_vmcnt<(NS - 2) * PER>();
+        } else {
+            static_for<0, NS - 2>([&](auto k_tag) {
+                constexpr int K = decltype(k_tag)::value;
+                if (tiles_after == K) wait_vmcnt<K * PER>();
+            });
+        }
     };
-    auto wait_outstanding = [&](int tiles_after) {
-        if (n_mine == PER) wait_tiles(tiles_after, std::integral_constant<int, PER>{});
-        else wait_tiles(tiles_after, std::integral_constant<int, (PER > 1 ? PER - 1 : 1)>{});
-    };
+    auto run_tiles = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int s = 0; s < NS - 1; ++s)
-        if (s < n_tiles) issue(k_begin + s * MBN, stage(s));   // tiles 0 .. NS-2
-    // Stage i % NS holds tile i.  Each iteration waits for tile i, then (after
-    // the barrier, when every wave has finished tile i-1) refills tile i-1's
-    // stage with tile i+NS-1.
+        if (s < n_tiles) issue(k_begin + s * MBN, stage(s));
     for (int t = 0; t < n_tiles; t += NS) {
-#pragma unroll
-        for (int s = 0; s < NS; ++s) {
-            const int i = t + s;
+        static_for<0, NS>([&](auto s_tag) {
+            constexpr int S = decltype(s_tag)::value;
+            const int i = t + S;
             if (i < n_tiles) {
-                const int issued = min(i + NS - 2, n_tiles - 1);   // last tile already in flight
-                wait_outstanding(issued - i);
-                __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
+                wait_outstanding(min(i + NS - 2, n_tiles - 1) - i);
+                __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));   // this wave's LDS reads done
                 bare_barrier();
                 const int ahead = i + NS - 1;
-                if (ahead < n_tiles) issue(k_begin + ahead * MBN, stage((s + NS - 1) % NS));
+                if (ahead < n_tiles) issue(k_begin + ahead * MBN, stage((S + NS - 1) % NS));
                 const int t0 = k_begin + i * MBN;
                 if (t0 + MBN > wmin || t0 < wsmax)
-                    compute(t0, stage(s), std::true_type{});
+                    compute(t0, stage(S), std::true_type{});
                 else
-                    compute(t0, stage(s), std::false_type{});
+                    compute(t0, stage(S), std::false_type{});
             }
-        }
+        });
     }
+    };
+    run_tiles();
+    // A spike anywhere in the workgroup: run the key range again with the
+    // exact maxima as references (they bound every score, so the second
+    // pass cannot spike).  Every wave has consumed every tile it waited for.
+    const bool wave_spike = __builtin_amdgcn_ballot_w64(spike) != 0;   // every lane votes
+    if (lane == 0) red[wave] = wave_spike;
+    __syncthreads();
+    bool again = false;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) again |= red[w] != 0;
+    __syncthreads();
+    if (again) {
+        zero_o();
+        l_run = 0.f;
+        m_run = m_seen;
+        run_tiles();
+    }
+
+    // The epilogue reads the accumulators: wait out the MFMA write latency
+    // first (the statements also keep those reads after the wait).
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+a"(o[0]), "+a"(o[1]), "+a"(o[2]), "+a"(o[3]), "+a"(o[4]),
+                 "+a"(o[5]), "+a"(o[6]), "+a"(o[7]));
+    asm volatile("" : "+a"(o[8]), "+a"(o[9]), "+a"(o[10]), "+a"(o[11]), "+a"(o[12]), "+a"(o[13]), "+a"(o[14]),
+                 "+a"(o[15]));
 
     const float l_tot = l_run + __shfl_xor(l_run, 32);
     if (!row_ok) return;
@@ -398,10 +417,10 @@ __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnAr
                 u32x2 w;
                 w[0] = bf_rne(o[db][4 * b] * inv) | (bf_rne(o[db][4 * b + 1] * inv) << 16);
                 w[1] = bf_rne(o[db][4 * b + 2] * inv) | (bf_rne(o[db][4 * b + 3] * inv) << 16);
-                *(u32x2*)(orow + vhalf * 256 + db * 32 + b * 8 + hl * 4) = w;
+                *(u32x2*)(orow + db * 32 + b * 8 + hl * 4) = w;
             }
         }
-        if (a.lse_out && hl == 0 && vhalf == 0) a.lse_out[((int64_t)layer * a.total_q + row) * H + head] = lse2 * kLn2;
+        if (a.lse_out && hl == 0) a.lse_out[((int64_t)layer * a.total_q + row) * H + head] = lse2 * kLn2;
     } else {
         const int64_t item = (((int64_t)split * a.n_layers + layer) * a.total_q + row) * H + head;
         float* wo = a.ws_o + item * DV;
@@ -411,17 +430,17 @@ __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnAr
             for (int b = 0; b < 4; ++b) {
                 f32x4 w = {o[db][4 * b] * inv, o[db][4 * b + 1] * inv, o[db][4 * b + 2] * inv,
                            o[db][4 * b + 3] * inv};
-                *(f32x4*)(wo + vhalf * 256 + db * 32 + b * 8 + hl * 4) = w;
+                *(f32x4*)(wo + db * 32 + b * 8 + hl * 4) = w;
             }
         }
-        if (hl == 0 && vhalf == 0) a.ws_lse[item] = lse2;
+        if (hl == 0) a.ws_lse[item] = lse2;
     }
 }
 
 }  // namespace
 
 hipError_t launch_attn_mla_bf16(const AttnArgs& a, const Plan& p, dim3 grid, hipStream_t stream) {
-    if (p.nw != kMlaWaves || p.ns != kMlaStages || p.BM != kMlaWaves / 2 * 32) return hipErrorInvalidValue;
+    if (p.nw != kMlaWaves || p.ns != kMlaStages || p.BM != kMlaWaves * 32) return hipErrorInvalidValue;
     if (a.block_table)
         hipLaunchKernelGGL((attn_mla_bf16_kernel<true>), grid, dim3(kMlaWaves * 64), 0, stream, a, p);
     else

@@ -303,15 +303,15 @@ def planned_splits(L, H, Hkv, d, dv, total_q, kv, variant=0, dtype=0):
 def test_split_planner_choices():
     """The planner weighs workgroup rounds over the 256 CUs (each with a fixed cost) against the
     combine pass's traffic: the 8B workload fills the GPU in one round (no split), the 32k prefill
-    and the MLA workload split 2 ways; launched one layer at a time they split 16, 2 and 8 ways
-    (each the measured best, or tied with it, on MI355X); short caches never split below 512 keys
-    per split."""
+    splits 2 ways and the MLA workload (128-row workgroups) 4 ways; launched one layer at a time
+    they split 16, 2 and 16 ways (each the measured best, or tied with it, on MI355X); short caches
+    never split below 512 keys per split."""
     assert planned_splits(32, 32, 8, 128, 128, 64, 8256) == 1
     assert planned_splits(28, 28, 4, 128, 128, 1024, 50176) == 2
-    assert planned_splits(27, 16, 1, 576, 512, 128, 32896, variant=1) == 2
+    assert planned_splits(27, 16, 1, 576, 512, 128, 32896, variant=1) == 4
     assert planned_splits(1, 32, 8, 128, 128, 64, 8256) == 16
     assert planned_splits(1, 28, 4, 128, 128, 1024, 50176) == 2
-    assert planned_splits(1, 16, 1, 576, 512, 128, 32896, variant=1) == 8
+    assert planned_splits(1, 16, 1, 576, 512, 128, 32896, variant=1) == 16
     assert planned_splits(1, 8, 2, 128, 128, 16, 300) == 1
     assert planned_splits(1, 8, 2, 128, 128, 16, 1000) == 1    # under 2 x 512 keys: no split
     assert planned_splits(1, 8, 2, 128, 128, 16, 4096) > 1     # one layer, one KV head pair: split to fill CUs

@@ -163,3 +163,51 @@ def test_fp32_ragged_split(splits, window):
                                               1 / np.sqrt(d), window=window)
             assert np.abs(got[l, rows] - want).max() <= 1e-5
             np.testing.assert_allclose(lse[l, rows], want_lse, rtol=1e-5, atol=1e-5)
+
+
+@pytest.mark.parametrize("scale", [0.0, -1 / 192 ** 0.5])
+def test_mla_zero_and_negative_scale(scale):
+    """Absorbed MLA attention with scale 0 (every visible slot weighs the same: the mean of the
+    visible latent rows) and a negative scale, one pass and split, against the oracle."""
+    L, H, n_q, kv = 2, 16, 7, 500
+    g = synth.Draws(41, "cpu")
+    q = host_bits(g.normal((L, n_q, H, 576)))
+    rows = host_bits(g.normal((L, 1, kv, 576)))
+    q_pos = np.array([0, 3, 31, 32, 250, 498, 499], np.int32)
+    for splits in (1, 3):
+        out = torch.zeros(L, n_q, H, 512, dtype=torch.bfloat16, device="cuda")
+        rd = dev(rows)
+        pkv.suffix_attention(dev(q), rd, rd[..., :512], out, torch.from_numpy(q_pos).cuda(),
+                             torch.tensor([kv], dtype=torch.int32, device="cuda"), scale, max_kv_len=kv,
+                             variant=pkv.PKV_ATTN_MLA, n_splits=splits)
+        torch.cuda.synchronize()
+        got = host_bits(out)
+        for l in range(L):
+            want, _ = oracle.attention(q[l], rows[l], rows[l][..., :512], q_pos, kv, scale)
+            log("  mla scale %g splits %d layer %d" % (scale, splits, l), check_attention_close(got[l], want))
+
+
+def test_mla_score_spike_reruns_the_key_range():
+    """A latent row whose k_pe (32x one row's q_pe) puts that row's score about 200 (log2 units) above
+    every score before it, past the fp32 range of a probability taken against the earlier maximum:
+    the workgroup must run its key range a second time with exact maxima.  The row returns that
+    slot's latent and the other rows still match the oracle."""
+    L, H, n_q, kv = 1, 16, 8, 900
+    g = synth.Draws(42, "cpu")
+    q = g.normal((L, n_q, H, 576))
+    rows = g.normal((L, 1, kv, 576))
+    rows[0, 0, 700, 512:] = (q[0, 5, 7, 512:].float() * 32).to(torch.bfloat16)
+    qh, rh = host_bits(q), host_bits(rows)
+    q_pos = np.arange(kv - n_q, kv, dtype=np.int32)
+    scale = 1 / 192 ** 0.5
+    for splits in (1, 2):
+        out = torch.zeros(L, n_q, H, 512, dtype=torch.bfloat16, device="cuda")
+        rd = rows.cuda()
+        pkv.suffix_attention(q.cuda(), rd, rd[..., :512], out, torch.from_numpy(q_pos).cuda(),
+                             torch.tensor([kv], dtype=torch.int32, device="cuda"), scale, max_kv_len=kv,
+                             variant=pkv.PKV_ATTN_MLA, n_splits=splits)
+        torch.cuda.synchronize()
+        got = host_bits(out)
+        want, _ = oracle.attention(qh[0], rh[0], rh[0][..., :512], q_pos, kv, scale)
+        log("  spike splits %d" % splits, check_attention_close(got[0], want))
+        np.testing.assert_allclose(bits_to_f64(got[0, 5, 7]), bits_to_f64(rh[0, 0, 700, :512]), atol=3e-2)
