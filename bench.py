@@ -291,6 +291,9 @@ class BatchedStep:
     def splice_bytes(self):
         return synth.batched_splice_bytes(self.bw, self.plan)
 
+    def splice_bytes_per_segment(self):
+        return synth.batched_splice_bytes_per_segment(self.bw, self.plan)
+
     def attn_flops(self):
         return synth.batched_attn_flops(self.bw, self.plan)
 
@@ -480,7 +483,7 @@ def cpu_baseline_batched(bw: synth.BatchedWorkload, budget_s: float):
                   "(evenly spaced) over %d slots in %.2f s, scaled to all sequences and layers by visible pairs"
                   % (passes, "/".join(str(sg["n_tokens"]) for sg in sq["segs"]), bw.n_layers, sample_bytes / 1e9,
                      t_splice, n_rows, bw.n_q, sq["kv_len"], t_attn),
-        "splice_us": round(synth.batched_splice_bytes(bw, plan) / (sample_bytes / t_splice) * 1e6, 1),
+        "splice_us": round(synth.batched_splice_bytes_per_segment(bw, plan) / (sample_bytes / t_splice) * 1e6, 1),
         "attention_us": round(attn_us_full, 1),
         "attention_kind": "extrapolated",
         "value_1thread": round(one1_bytes / t_one1 / 1e9, 4),
@@ -674,6 +677,11 @@ def measure(name, args, flush, stream, first):
         "roofline": splice_roof if s_ms >= a_ms else attn_roof,
         "roofline_kernels": [splice_roof, attn_roof],
     })
+    if hasattr(step, "splice_bytes_per_segment"):
+        # the same splice counted with one source read per segment (each sequence spliced on its own)
+        b = step.splice_bytes_per_segment()
+        res["splice_bytes_per_segment_reads"] = b
+        res["splice"]["gbps_per_segment_reads"] = round(b / (s_ms * 1e-3) / 1e9, 1)
 
     # Warm: the same steps back to back, no flush (the attention finds part of the splice's
     # writes in the last-level cache).

@@ -52,7 +52,8 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kUnroll = 1;         // rows whose loads are issued before any is used
 constexpr int kRowsPerBlock = 1;   // (layer, kv_head) rows per block
 constexpr int kBlock = 256;        // threads per block
-constexpr int kSegTiles = 32;      // segment mode: token-tile blocks per (row group, segment)
+constexpr int kSegTiles = 8;       // segment mode: token-tile blocks per (row group, segment)
+constexpr int kSegAhead = 4;       // segment mode: tiles whose loads are issued before the first store
 constexpr int kHalf = 0;
 constexpr int kWave = 64;
 constexpr int kXcds = 8;
@@ -67,6 +68,8 @@ struct Geo {
     int lanes_k, lanes_v, lanes, tok_per_block, rows_per_block;
     int rope_c0, rope_nc, n_kc, n_vc, n_rows, n_pairs;
     int xcd_tiles;          // tiles per XCD when the tile count divides by 8, else 0
+    int seg_xcd_rows;       // segment mode, 1-D grid: row groups per XCD (0: 3-D grid)
+    int seg_n, seg_tile_blocks;   // segment mode, 1-D grid: segments, tile blocks
     uint32_t lanes_magic;   // ceil(2^32 / lanes)
     double rho[7];          // theta^(-2*2^b/rope_dim), b = 0..6
 };
@@ -213,8 +216,28 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
     // blocks, row groups) with the segment the fastest axis, so the blocks of
     // all segments at one (tile block, row) are dispatched together and
     // segments that read the same source chunk (a shared skill) find it in the
-    // caches.
-    const int grp = SEG ? blockIdx.z : blockIdx.y;
+    // caches.  When the row groups divide evenly over the XCDs, segment mode
+    // runs on a 1-D grid whose ids are dealt to the XCDs round-robin: XCD x
+    // takes row groups x*seg_xcd_rows .. and, within them, the same
+    // (segment fastest) order, so every read of one source chunk goes through
+    // one XCD's L2 and only the first reaches memory.
+    int grp = blockIdx.y, seg_i = 0, tile_blk = 0, tile_blocks = 1;
+    if constexpr (SEG) {
+        if (g.seg_xcd_rows) {
+            const uint32_t id = blockIdx.x;
+            const uint32_t slot = id / kXcds;
+            seg_i = (int)(slot % (uint32_t)g.seg_n);
+            const uint32_t rest = slot / (uint32_t)g.seg_n;
+            tile_blk = (int)(rest % (uint32_t)g.seg_tile_blocks);
+            grp = (int)(id % kXcds) * g.seg_xcd_rows + (int)(rest / (uint32_t)g.seg_tile_blocks);
+            tile_blocks = g.seg_tile_blocks;
+        } else {
+            seg_i = blockIdx.x;
+            tile_blk = blockIdx.y;
+            tile_blocks = gridDim.y;
+            grp = blockIdx.z;
+        }
+    }
     const uint32_t tid = threadIdx.x;
     const uint32_t tl = g.lanes == 1 ? tid : __umulhi(tid, g.lanes_magic);   // tid / lanes, exact here
     const int lane = (int)(tid - tl * (uint32_t)g.lanes);
@@ -227,7 +250,7 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
     SpliceSegment sg{};
     int64_t n_tok = a.n_tokens;
     if constexpr (SEG) {
-        sg = a.segs[blockIdx.x];
+        sg = a.segs[seg_i];
         n_tok = sg.n_tokens;
     }
 
@@ -274,157 +297,176 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
     const int last_head = (r1 - 1) - last_layer * a.n_kv_heads;
 
     float cs[CE], sn[CE];
-    bool have_coef = false;
-
-    for (uint32_t step = 0;; ++step) {
-        // Token tile.  Single chunk: one tile per block; workgroups are dealt to
-        // the XCDs round-robin, so when the tile count divides evenly the tiles
-        // are renumbered to give each XCD one contiguous range of tokens.
-        uint32_t tile;
-        if constexpr (SEG) {
-            tile = blockIdx.y + step * gridDim.y;
-            if ((int64_t)tile * g.tok_per_block >= n_tok) break;   // uniform over the block
-        } else {
-            tile = blockIdx.x;
-            if (g.xcd_tiles) tile = (tile % kXcds) * g.xcd_tiles + tile / kXcds;
-        }
-        const int64_t t = (int64_t)tile * g.tok_per_block + tl;
-
-        // Loads go out in the order their results are needed: positions, then
-        // the K/V rows.  Memory counters retire in order, so waiting for the
-        // positions (and, on the first tile, the frequency) leaves the K/V
-        // loads in flight while the coefficients are formed.  Lanes and rows
-        // without work load from a clamped, in-range address and store
-        // nothing; they stay to the end because the wave shares its
-        // coefficients through shuffles.
-        int64_t src_slot, dst_slot = -1, delta = 0;
-        const bool present = in_tile && t < n_tok;   // a token of the chunk (or segment)
-        bool active;                                 // ... whose source row can be read
-        int32_t dp = 0, spos = 0, dslot = 0;
-        if constexpr (SEG) {
-            src_slot = sg.src_slot0 + t;
-            active = present && src_slot >= 0 && src_slot < a.n_tokens;
-            const int64_t p = (int64_t)sg.dst_pos0 + t;
-            if (p >= 0 && p < sg.dst_seq_len) dst_slot = sg.dst_seq_base + p;
-            delta = (int64_t)sg.dst_pos0 - (int64_t)sg.src_pos0;
-            if (!active) src_slot = 0;
-        } else {
-            active = present;
-            src_slot = active ? t : a.n_tokens - 1;
-            dp = a.dst_pos[src_slot];
-            spos = a.src_pos[src_slot];
-            if (a.dst_slot) dslot = a.dst_slot[src_slot];
-        }
-        const char* sbase = src_t + src_slot * s2 * EB;
-
-        int layer = layer0, head = head0;
-        u32x4 va[kUnroll], vb[kUnroll];
-        int64_t doff[kUnroll];
-        auto load_rows = [&](int r) __attribute__((always_inline)) {
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                const bool in = r + u < r1;
-                const int l = in ? layer : last_layer, h = in ? head : last_head;
-                doff[u] = ((int64_t)l * d0 + (int64_t)h * d1) * EB;
-                const char* sp = sbase + ((int64_t)l * s0 + (int64_t)h * s1) * EB;
-                if constexpr (SEG) {
-                    va[u] = ld16_cached(sp);
-                    vb[u] = ld16_cached(sp + ob);
-                } else {
-                    va[u] = ld16(sp);
-                    vb[u] = ld16(sp + ob);
-                }
-                if (++head == a.n_kv_heads) {
-                    head = 0;
-                    ++layer;
-                }
-            }
-        };
-        load_rows(r0);
-
-        if constexpr (!SEG) {
-            dst_slot = a.dst_slot ? dslot : dp;   // slots follow positions unless given
-            delta = (int64_t)dp - (int64_t)spos;
-        }
-        const bool valid = dst_slot >= 0 && dst_slot < a.dst_capacity;
-        const bool work = active && valid;
-        // Paged destination: the slot's page id is read from an in-range entry
-        // for every lane (no branch, so the wait for it stays with the K/V
-        // wait before the stores); a page outside the pool skips the token.
-        int64_t dst_row = dst_slot;
-        bool page_ok = true;
-        if constexpr (PAGED) {
-            const int64_t pidx = work ? dst_slot >> a.page_shift : 0;
-            const int32_t* table = !is_k && a.dst_v_pages ? a.dst_v_pages : a.dst_pages;
-            const int32_t page = table[pidx];
-            page_ok = page >= 0 && page < a.n_pages;
-            dst_row = (int64_t)page * dpg + (dst_slot & ((1 << a.page_shift) - 1)) * d2;
-        } else {
-            dst_row = dst_slot * d2;
-        }
-
-        // Rotation coefficients.  When every working lane of the wave has the
-        // same delta (always so in segment mode; so for a contiguous chunk in
-        // token mode), lane j evaluates pair j once and rotary lanes gather
-        // theirs by shuffle; otherwise each rotary lane evaluates its own CE
-        // pairs.  Segment mode forms them once per block.
-        bool rot = rope;
-        if (!SEG || !have_coef) {
-            const int32_t d_ref = __shfl((int32_t)delta, 0);
-            const bool uniform = __all(!work || delta == (int64_t)d_ref) && g.n_pairs <= kWave;
-            if (uniform) {
-                if (d_ref != 0) {
-                    float c1 = 1.0f, s1v = 0.0f;
-                    const int j = __lane_id();
-                    if (j < g.n_pairs) delta_sincos(d_ref, TAB ? w_lo : pair_omega(j, g), c1, s1v);
-#pragma unroll
-                    for (int e = 0; e < CE; ++e) {
-                        const int src = rope ? lane_pair<CE, STYLE>(lane, e, half_r) : 0;
-                        cs[e] = __shfl(c1, src);
-                        sn[e] = __shfl(s1v, src);
-                    }
-                }
-            } else if constexpr (TAB) {
-                // every lane takes part in the shuffles (the branch is wave-uniform)
-                double wp[CE];
+    // Rotation coefficients of this lane's CE pairs for the lane's delta.
+    // When every working lane of the wave has the same delta (always so in
+    // segment mode; so for a contiguous chunk in token mode), lane j
+    // evaluates pair j once and rotary lanes gather theirs by shuffle;
+    // otherwise each rotary lane evaluates its own CE pairs.  Every lane of
+    // the wave calls this (the shuffles need them all).
+    auto coefficients = [&](int64_t delta, bool work) __attribute__((always_inline)) {
+        const int32_t d_ref = __shfl((int32_t)delta, 0);
+        const bool uniform = __all(!work || delta == (int64_t)d_ref) && g.n_pairs <= kWave;
+        if (uniform) {
+            if (d_ref != 0) {
+                float c1 = 1.0f, s1v = 0.0f;
+                const int j = __lane_id();
+                if (j < g.n_pairs) delta_sincos(d_ref, TAB ? w_lo : pair_omega(j, g), c1, s1v);
 #pragma unroll
                 for (int e = 0; e < CE; ++e) {
-                    const int pr = rope ? lane_pair<CE, STYLE>(lane, e, half_r) : 0;
-                    const double lo = __shfl(w_lo, pr & (kWave - 1)), hi = __shfl(w_hi, pr & (kWave - 1));
-                    wp[e] = pr < kWave ? lo : hi;
+                    const int src = rope ? lane_pair<CE, STYLE>(lane, e, half_r) : 0;
+                    cs[e] = __shfl(c1, src);
+                    sn[e] = __shfl(s1v, src);
                 }
-                if (rope && delta != 0) {
-#pragma unroll
-                    for (int e = 0; e < CE; ++e) delta_sincos(delta, wp[e], cs[e], sn[e]);
-                }
-            } else if (rope && delta != 0) {
-#pragma unroll
-                for (int e = 0; e < CE; ++e)
-                    delta_sincos(delta, pair_omega(lane_pair<CE, STYLE>(lane, e, half_r), g), cs[e], sn[e]);
             }
-            have_coef = true;
+        } else if constexpr (TAB) {
+            // every lane takes part in the shuffles (the branch is wave-uniform)
+            double wp[CE];
+#pragma unroll
+            for (int e = 0; e < CE; ++e) {
+                const int pr = rope ? lane_pair<CE, STYLE>(lane, e, half_r) : 0;
+                const double lo = __shfl(w_lo, pr & (kWave - 1)), hi = __shfl(w_hi, pr & (kWave - 1));
+                wp[e] = pr < kWave ? lo : hi;
+            }
+            if (rope && delta != 0) {
+#pragma unroll
+                for (int e = 0; e < CE; ++e) delta_sincos(delta, wp[e], cs[e], sn[e]);
+            }
+        } else if (rope && delta != 0) {
+#pragma unroll
+            for (int e = 0; e < CE; ++e)
+                delta_sincos(delta, pair_omega(lane_pair<CE, STYLE>(lane, e, half_r), g), cs[e], sn[e]);
         }
-        rot = rope && delta != 0;
+    };
 
-        if (work && page_ok) {
-            char* dbase = dst_t + dst_row * EB;
-            for (int r = r0;;) {
+    if constexpr (SEG) {
+        // Segment mode: one (layer, head) row per block and one delta per
+        // segment, so the coefficients are formed once.  The block's tiles
+        // (tile_blk, tile_blk + tile_blocks, ...) go kSegAhead at a time:
+        // the loads of all of them are issued before the first store, so each
+        // wave keeps kSegAhead tiles of loads in flight.  Lanes without a
+        // readable source row load nothing.
+        static_assert(kRowsPerBlock == 1, "segment mode handles one row per block");
+        const char* const srow = src_t + ((int64_t)layer0 * s0 + (int64_t)head0 * s1) * EB;
+        char* const drow = dst_t + ((int64_t)layer0 * d0 + (int64_t)head0 * d1) * EB;
+        const int64_t delta = (int64_t)sg.dst_pos0 - (int64_t)sg.src_pos0;
+        coefficients(delta, true);
+        const bool rot = rope && delta != 0;
+        for (uint32_t step = 0;; step += kSegAhead) {
+            if ((int64_t)(tile_blk + step * tile_blocks) * g.tok_per_block >= n_tok) break;   // uniform
+            u32x4 va[kSegAhead], vb[kSegAhead];
+            int64_t dst_row[kSegAhead];
+            bool present[kSegAhead], work[kSegAhead];
 #pragma unroll
-                for (int u = 0; u < kUnroll; ++u) {
-                    if (r + u < r1) {
-                        if (rot) rotate_chunks<EB, STYLE>(va[u], vb[u], cs, sn);
-                        st16(dbase + doff[u], va[u]);
-                        st16(dbase + doff[u] + ob, vb[u]);
-                    }
+            for (int u = 0; u < kSegAhead; ++u) {
+                const int64_t t = (int64_t)(tile_blk + (step + u) * tile_blocks) * g.tok_per_block + tl;
+                present[u] = in_tile && t < n_tok;
+                const int64_t src_slot = sg.src_slot0 + t;
+                const bool active = present[u] && src_slot >= 0 && src_slot < a.n_tokens;
+                const int64_t p = (int64_t)sg.dst_pos0 + t;
+                const int64_t dst_slot = p >= 0 && p < sg.dst_seq_len ? sg.dst_seq_base + p : -1;
+                work[u] = active && dst_slot >= 0 && dst_slot < a.dst_capacity;
+                dst_row[u] = dst_slot * d2;
+                va[u] = vb[u] = u32x4{0u, 0u, 0u, 0u};
+                if (active) {
+                    const char* sp = srow + src_slot * s2 * EB;
+                    va[u] = ld16_cached(sp);
+                    vb[u] = ld16_cached(sp + ob);
                 }
-                r += kUnroll;
-                if (r >= r1) break;
-                load_rows(r);
+            }
+#pragma unroll
+            for (int u = 0; u < kSegAhead; ++u) {
+                if (work[u]) {
+                    if (rot) rotate_chunks<EB, STYLE>(va[u], vb[u], cs, sn);
+                    char* dp = drow + dst_row[u] * EB;
+                    st16(dp, va[u]);
+                    st16(dp + ob, vb[u]);
+                }
+                if (present[u] && !work[u] && lane == 0 && grp == 0 && a.err_flag) atomicOr(a.err_flag, 1);
             }
         }
-        if (present && !(work && page_ok) && lane == 0 && grp == 0 && a.err_flag) atomicOr(a.err_flag, 1);
-        if constexpr (!SEG) break;
+        return;
     }
+
+    // Token mode: one tile per block.  Workgroups are dealt to the XCDs
+    // round-robin, so when the tile count divides evenly the tiles are
+    // renumbered to give each XCD one contiguous range of tokens.
+    uint32_t tile = blockIdx.x;
+    if (g.xcd_tiles) tile = (tile % kXcds) * g.xcd_tiles + tile / kXcds;
+    const int64_t t = (int64_t)tile * g.tok_per_block + tl;
+
+    // Loads go out in the order their results are needed: positions, then
+    // the K/V rows.  Memory counters retire in order, so waiting for the
+    // positions (and the frequencies) leaves the K/V loads in flight while
+    // the coefficients are formed.  Lanes and rows without work load from a
+    // clamped, in-range address and store nothing; they stay to the end
+    // because the wave shares its coefficients through shuffles.
+    const bool present = in_tile && t < n_tok;   // a token of the chunk
+    const bool active = present;
+    const int64_t src_slot = active ? t : a.n_tokens - 1;
+    const int32_t dp = a.dst_pos[src_slot];
+    const int32_t spos = a.src_pos[src_slot];
+    const int32_t dslot = a.dst_slot ? a.dst_slot[src_slot] : 0;
+    const char* sbase = src_t + src_slot * s2 * EB;
+
+    int layer = layer0, head = head0;
+    u32x4 va[kUnroll], vb[kUnroll];
+    int64_t doff[kUnroll];
+    auto load_rows = [&](int r) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const bool in = r + u < r1;
+            const int l = in ? layer : last_layer, h = in ? head : last_head;
+            doff[u] = ((int64_t)l * d0 + (int64_t)h * d1) * EB;
+            const char* sp = sbase + ((int64_t)l * s0 + (int64_t)h * s1) * EB;
+            va[u] = ld16(sp);
+            vb[u] = ld16(sp + ob);
+            if (++head == a.n_kv_heads) {
+                head = 0;
+                ++layer;
+            }
+        }
+    };
+    load_rows(r0);
+
+    const int64_t dst_slot = a.dst_slot ? dslot : dp;   // slots follow positions unless given
+    const int64_t delta = (int64_t)dp - (int64_t)spos;
+    const bool valid = dst_slot >= 0 && dst_slot < a.dst_capacity;
+    const bool work = active && valid;
+    // Paged destination: the slot's page id is read from an in-range entry
+    // for every lane (no branch, so the wait for it stays with the K/V
+    // wait before the stores); a page outside the pool skips the token.
+    int64_t dst_row = dst_slot;
+    bool page_ok = true;
+    if constexpr (PAGED) {
+        const int64_t pidx = work ? dst_slot >> a.page_shift : 0;
+        const int32_t* table = !is_k && a.dst_v_pages ? a.dst_v_pages : a.dst_pages;
+        const int32_t page = table[pidx];
+        page_ok = page >= 0 && page < a.n_pages;
+        dst_row = (int64_t)page * dpg + (dst_slot & ((1 << a.page_shift) - 1)) * d2;
+    } else {
+        dst_row = dst_slot * d2;
+    }
+
+    coefficients(delta, work);
+    const bool rot = rope && delta != 0;
+
+    if (work && page_ok) {
+        char* dbase = dst_t + dst_row * EB;
+        for (int r = r0;;) {
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                if (r + u < r1) {
+                    if (rot) rotate_chunks<EB, STYLE>(va[u], vb[u], cs, sn);
+                    st16(dbase + doff[u], va[u]);
+                    st16(dbase + doff[u] + ob, vb[u]);
+                }
+            }
+            r += kUnroll;
+            if (r >= r1) break;
+            load_rows(r);
+        }
+    }
+    if (present && !(work && page_ok) && lane == 0 && grp == 0 && a.err_flag) atomicOr(a.err_flag, 1);
 }
 
 template <int EB, int STYLE>
@@ -491,7 +533,14 @@ hipError_t launch_splice(const SpliceArgs& a, hipStream_t stream) {
 
     for (int b = 0; b < kPairBits; ++b) g.rho[b] = pow(a.theta, -2.0 * (double)(1 << b) / (double)a.rope_dim);
 
-    dim3 grid = seg ? dim3((unsigned)nz, (unsigned)n_tiles, (unsigned)n_groups)
+    // Segment mode with row groups divisible by the XCD count: 1-D grid
+    // (decoded in the kernel so that each XCD owns whole row groups).
+    const int64_t seg_1d = nz * n_tiles * n_groups;
+    g.seg_xcd_rows = seg && n_groups % kXcds == 0 && seg_1d <= 0x7fffffff ? (int)(n_groups / kXcds) : 0;
+    g.seg_n = (int)nz;
+    g.seg_tile_blocks = (int)n_tiles;
+    dim3 grid = seg ? (g.seg_xcd_rows ? dim3((unsigned)seg_1d, 1u, 1u)
+                                      : dim3((unsigned)nz, (unsigned)n_tiles, (unsigned)n_groups))
                     : dim3((unsigned)n_tiles, (unsigned)n_groups, 1u);
     dim3 block((unsigned)kBlock);
     if (a.elem_bytes == 2)

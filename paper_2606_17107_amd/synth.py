@@ -317,7 +317,20 @@ def batched_segments(plan):
 
 
 def batched_splice_bytes(bw: BatchedWorkload, plan) -> int:
-    """Algorithmic bytes of the batched splice: every spliced token's K and V rows read once and written once."""
+    """Algorithmic bytes of the batched splice: the library's K and V rows read once (every distinct
+    source slot, however many sequences splice it) and every spliced token's K and V rows written once,
+    the least HBM traffic the composition needs."""
+    src = set()
+    for sq in plan["seqs"]:
+        for sg in sq["segs"]:
+            src.update(range(sg["src_slot0"], sg["src_slot0"] + sg["n_tokens"]))
+    written = sum(sg["n_tokens"] for sq in plan["seqs"] for sg in sq["segs"])
+    return 2 * (len(src) + written) * bw.n_layers * bw.n_kv_heads * bw.head_dim * 2
+
+
+def batched_splice_bytes_per_segment(bw: BatchedWorkload, plan) -> int:
+    """Bytes of the batched splice with every segment reading its own source (each spliced token's K and
+    V rows read once and written once): the work of splicing each sequence on its own."""
     tokens = sum(sg["n_tokens"] for sq in plan["seqs"] for sg in sq["segs"])
     return 2 * 2 * tokens * bw.n_layers * bw.n_kv_heads * bw.head_dim * 2
 

@@ -322,6 +322,40 @@ def test_batched_out_of_range_segment_flagged():
     check_rotated_keys(gk, ok, 0, bw.head_dim, 0)
 
 
+def test_batched_long_segments_whole_rows_per_xcd():
+    """8 (layer, head) rows (the launch then gives each XCD whole rows) and segments long enough that a
+    block walks five tiles of 16 tokens (two batches of up to four in-flight tiles); three sequences
+    share each skill."""
+    bw = synth.BatchedWorkload(n_seqs=3, skills=(40, 700, 2100), ctx_min=3000, ctx_max=3400, src_pos_max=300,
+                               n_layers=4, n_heads=8, n_kv_heads=2, head_dim=128, n_q=19)
+    plan = synth.batched_plan(bw, seed=4)
+    case = batched_inputs(bw, plan, seed=5)
+    segs = segments_of(plan)
+    gk, gv, flag = run_batched(bw, plan, case, segs, max(s["n_tokens"] for s in segs))
+    assert flag == 0
+    ok, ov = oracle_batched(bw, plan, case, segs)
+    np.testing.assert_array_equal(gv, ov)
+    check_rotated_keys(gk, ok, 0, bw.head_dim, 0)
+
+
+def test_batched_source_out_of_range():
+    """A segment whose source slots lie past the end of the source tensor writes nothing and sets the
+    flag; a segment straddling the end writes only its in-range tokens."""
+    bw = synth.BatchedWorkload(n_seqs=3, skills=(40, 100, 257), ctx_min=600, ctx_max=900, src_pos_max=300,
+                               n_layers=4, n_heads=8, n_kv_heads=2, head_dim=128, n_q=19)
+    plan = synth.batched_plan(bw, seed=1)
+    case = batched_inputs(bw, plan, seed=2)
+    n_src = case["skill_k"].shape[2]
+    segs = segments_of(plan)[:1]
+    outside = dict(segments_of(plan)[8], src_slot0=n_src + 10)
+    straddle = dict(segments_of(plan)[4], src_slot0=n_src - 7)
+    gk, gv, flag = run_batched(bw, plan, case, segs + [outside, straddle], 300)
+    assert flag == 1
+    ok, ov = oracle_batched(bw, plan, case, segs + [dict(straddle, n_tokens=7)])
+    np.testing.assert_array_equal(gv, ov)
+    check_rotated_keys(gk, ok, 0, bw.head_dim, 0)
+
+
 # ---- full-size workloads (the launch configuration the benchmark times) -----
 
 def full_size(w, layers=None, seed=0):
