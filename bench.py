@@ -516,6 +516,50 @@ def device_copy_gbps(nbytes: int = 1 << 30, reps: int = 10) -> float:
     return best
 
 
+STREAM_COPY_LIB = os.path.join(ROOT, "paper_2606_17107_amd", "libpkv_copy.so")
+
+
+def stream_copy(dst: torch.Tensor, src: torch.Tensor, stream) -> None:
+    """The stream-copy reference kernel (paper_2606_17107_amd/probe/stream_copy.hip): the splice's
+    access pattern without its arithmetic."""
+    import ctypes
+
+    if not os.path.exists(STREAM_COPY_LIB):
+        raise RuntimeError("%s is missing: run __graft_entry__.build()" % STREAM_COPY_LIB)
+    lib = ctypes.CDLL(STREAM_COPY_LIB)
+    fn = lib.pkv_stream_copy
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    fn.restype = ctypes.c_int
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nbytes:
+        raise ValueError("stream_copy: size mismatch")
+    rc = fn(dst.data_ptr(), src.data_ptr(), nbytes, stream)
+    if rc != 0:
+        raise RuntimeError("pkv_stream_copy failed (%d)" % rc)
+
+
+def stream_copy_gbps(flush, nbytes: int = 512 << 20, reps: int = 10) -> float:
+    """Rate (bytes read + written per second) of the stream-copy reference kernel, every launch cold
+    (after the flush) like the splice's: the ceiling of the splice's memory traffic."""
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    st = torch.cuda.current_stream()
+    for _ in range(3):
+        stream_copy(dst, src, st.cuda_stream)
+    ts = []
+    for _ in range(reps):
+        flush()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(st)
+        stream_copy(dst, src, st.cuda_stream)
+        b.record(st)
+        torch.cuda.synchronize()
+        ts.append(a.elapsed_time(b))
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2 * nbytes / (sum(ts) / len(ts) * 1e-3) / 1e9
+
+
 def source_hash(files):
     """Hash of the kernel sources a counter measurement was taken against."""
     import hashlib
@@ -806,8 +850,10 @@ def main():
         torch.cuda.empty_cache()
     t_gpu = time.perf_counter() - t_gpu
     cp = device_copy_gbps()
+    sc = stream_copy_gbps(flush)
     for r in configs.values():
         r["splice"]["of_device_copy"] = round(r["splice"]["gbps"] / cp, 4)
+        r["splice"]["of_stream_copy"] = round(r["splice"]["gbps"] / sc, 4)
     if not args.no_cpu_baseline:
         for name in names:
             log("timing the CPU oracle:", name)
@@ -837,6 +883,7 @@ def main():
         "roofline": head["roofline"],
         "roofline_kernels": head["roofline_kernels"],
         "device_copy_gbps": round(cp, 1),
+        "stream_copy_gbps": round(sc, 1),
         "gpu_wall_s": round(t_gpu, 2),
         "configs": configs,
     }

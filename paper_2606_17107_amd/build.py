@@ -78,7 +78,26 @@ def build(verbose: bool = False) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)
     os.replace(tmp, LIB)
+    build_copy(verbose)
     return LIB
+
+
+COPY_SRC = os.path.join(PKG, "probe", "stream_copy.hip")
+COPY_LIB = os.path.join(PKG, "libpkv_copy.so")
+
+
+def build_copy(verbose: bool = False) -> str:
+    """The stream-copy reference kernel the benchmark times beside the splice (its own library)."""
+    tmp = COPY_LIB + ".tmp%d" % os.getpid()
+    cmd = [hipcc()] + compile_flags() + ["-shared", COPY_SRC, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    out = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)
+    if out.returncode != 0:
+        sys.stderr.write(out.stdout.decode(errors="replace"))
+        raise RuntimeError("hipcc failed for " + COPY_SRC)
+    os.replace(tmp, COPY_LIB)
+    return COPY_LIB
 
 
 if __name__ == "__main__":

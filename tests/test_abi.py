@@ -323,3 +323,14 @@ def test_split_planner_fp32():
     assert planned_splits(1, 4, 2, 64, 64, 16, 100, dtype=1) == 1       # under 2 x 64 keys
     assert planned_splits(1, 4, 2, 64, 64, 16, 100000, dtype=1) == 32   # capped
     assert planned_splits(8, 32, 8, 128, 128, 64, 4096, dtype=1) == 1   # 256 workgroups already
+
+
+def test_stream_copy_library_exports():
+    """The stream-copy reference library (timed by bench.py beside the splice) is built and exports its
+    one entry point."""
+    import ctypes
+    import os
+    from paper_2606_17107_amd import build as B
+    assert os.path.exists(B.COPY_LIB)
+    lib = ctypes.CDLL(B.COPY_LIB)
+    assert hasattr(lib, "pkv_stream_copy")
