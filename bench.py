@@ -561,27 +561,29 @@ def stream_copy_gbps(flush, nbytes: int = 512 << 20, reps: int = 10) -> float:
 
 
 def source_hash(files):
-    """Hash of the kernel sources a counter measurement was taken against."""
+    """Hash of the kernel sources a counter measurement was taken against, and of the compiler
+    options the first of them (the kernel's translation unit) is built with."""
     import hashlib
+
+    from paper_2606_17107_amd import build as B
 
     h = hashlib.sha256()
     for f in files:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
+    flags = B.compile_flags() + B.FILE_FLAGS.get(os.path.basename(files[0]), [])
+    h.update(" ".join(f.replace(ROOT, "") for f in flags).encode())
     return h.hexdigest()[:16]
 
 
-KERNEL_SOURCES = {   # the sources and compiler options each kernel is built from
-    "splice_kernel": ["paper_2606_17107_amd/csrc/splice.hip", "paper_2606_17107_amd/csrc/pkv_internal.h",
-                      "paper_2606_17107_amd/build.py"],
+KERNEL_SOURCES = {   # the kernel's translation unit first, then the headers it includes
+    "splice_kernel": ["paper_2606_17107_amd/csrc/splice.hip", "paper_2606_17107_amd/csrc/pkv_internal.h"],
     "attn_gqa_bf16": ["paper_2606_17107_amd/csrc/attn_gqa_bf16.hip", "paper_2606_17107_amd/csrc/attn_common.h",
-                      "paper_2606_17107_amd/csrc/attention.hip", "paper_2606_17107_amd/csrc/pkv_internal.h",
-                      "paper_2606_17107_amd/build.py"],
+                      "paper_2606_17107_amd/csrc/attention.hip", "paper_2606_17107_amd/csrc/pkv_internal.h"],
     "attn_mla_bf16": ["paper_2606_17107_amd/csrc/attn_mla_bf16.hip", "paper_2606_17107_amd/csrc/attn_common.h",
-                      "paper_2606_17107_amd/csrc/attention.hip", "paper_2606_17107_amd/csrc/pkv_internal.h",
-                      "paper_2606_17107_amd/build.py"],
+                      "paper_2606_17107_amd/csrc/attention.hip", "paper_2606_17107_amd/csrc/pkv_internal.h"],
     "attn_gqa_f32": ["paper_2606_17107_amd/csrc/attention.hip", "paper_2606_17107_amd/csrc/attn_common.h",
-                     "paper_2606_17107_amd/csrc/pkv_internal.h", "paper_2606_17107_amd/build.py"],
+                     "paper_2606_17107_amd/csrc/pkv_internal.h"],
 }
 
 
