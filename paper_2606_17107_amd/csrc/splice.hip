@@ -53,7 +53,7 @@ constexpr int kUnroll = 1;         // rows whose loads are issued before any is 
 constexpr int kRowsPerBlock = 1;   // (layer, kv_head) rows per block
 constexpr int kBlock = 256;        // threads per block
 constexpr int kSegTiles = 8;       // segment mode: token-tile blocks per (row group, segment)
-constexpr int kSegAhead = 4;       // segment mode: tiles whose loads are issued before the first store
+constexpr int kSegAhead = 6;       // segment mode: tiles whose loads are issued before the first store
 constexpr int kHalf = 0;
 constexpr int kWave = 64;
 constexpr int kXcds = 8;
