@@ -475,13 +475,11 @@ hipError_t launch_typed(const SpliceArgs& a, const Geo& g, dim3 grid, dim3 block
         if (a.segs || a.omega) return hipErrorInvalidValue;
         const FreqArg<false> ft;
         hipLaunchKernelGGL((splice_kernel<EB, STYLE, false, false, true>), grid, block, 0, st, a, g, ft);
-    } else if (a.omega) {
+    } else if (a.omega) {   // explicit frequencies: per-token mode
+        if (a.segs) return hipErrorInvalidValue;
         FreqArg<true> ft;
         for (int i = 0; i < (1 << kPairBits); ++i) ft.w[i] = i < g.n_pairs ? a.omega[i] : 0.0;
-        if (a.segs)
-            hipLaunchKernelGGL((splice_kernel<EB, STYLE, true, true, false>), grid, block, 0, st, a, g, ft);
-        else
-            hipLaunchKernelGGL((splice_kernel<EB, STYLE, false, true, false>), grid, block, 0, st, a, g, ft);
+        hipLaunchKernelGGL((splice_kernel<EB, STYLE, false, true, false>), grid, block, 0, st, a, g, ft);
     } else {
         const FreqArg<false> ft;
         if (a.segs)

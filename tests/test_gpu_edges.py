@@ -130,15 +130,16 @@ def test_sequence_without_slots():
         check_attention_close(got[0, rows], want)
 
 
-@pytest.mark.parametrize("splits,window", [(0, 0), (0, 150), (5, 150)])
-def test_fp32_ragged_split(splits, window):
+@pytest.mark.parametrize("splits,window,d", [(0, 0, 64), (0, 150, 64), (5, 150, 64), (0, 0, 128), (3, 150, 128)])
+def test_fp32_ragged_split(splits, window, d):
     """fp32 attention over ragged sequences, split over the keys (0: the planner's count) with and
-    without a sliding window, at fp32 tolerance against the oracle."""
-    H, Hkv, d, L = 4, 2, 64, 2
+    without a sliding window, at fp32 tolerance against the oracle; both head sizes of the fp32
+    kernel."""
+    H, Hkv, L = 4, 2, 2
     nqs, kvls = [7, 16, 3], [530, 300, 700]
     caps = [kl + 5 for kl in kvls]
     bases = np.concatenate([[0], np.cumsum(caps)[:-1]]).astype(np.int64)
-    g = synth.Draws(40 + splits + window, "cpu")
+    g = synth.Draws(40 + splits + window + d, "cpu")
     k = g.normal((L, Hkv, int(sum(caps)), d), torch.float32).numpy()
     v = g.normal((L, Hkv, int(sum(caps)), d), torch.float32).numpy()
     q = g.normal((L, sum(nqs), H, d), torch.float32).numpy()
@@ -146,7 +147,7 @@ def test_fp32_ragged_split(splits, window):
     cu = np.concatenate([[0], np.cumsum(nqs)]).astype(np.int32)
     out = torch.zeros(L, sum(nqs), H, d, dtype=torch.float32, device="cuda")
     lse = torch.zeros(L, sum(nqs), H, dtype=torch.float32, device="cuda")
-    log("fp32 ragged, splits %d, window %d" % (splits, window))
+    log("fp32 ragged, splits %d, window %d, d %d" % (splits, window, d))
     pkv.suffix_attention(torch.from_numpy(q).cuda(), torch.from_numpy(k).cuda(), torch.from_numpy(v).cuda(), out,
                          torch.from_numpy(q_pos).cuda(), torch.tensor(kvls, dtype=torch.int32, device="cuda"),
                          1 / np.sqrt(d), max_kv_len=max(kvls), n_seqs=3, cu_q=torch.from_numpy(cu).cuda(),
