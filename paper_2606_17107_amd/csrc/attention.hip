@@ -176,49 +176,54 @@ __global__ __launch_bounds__(256) void attn_gqa_f32(AttnArgs a, Plan p) {
 }
 
 // Merge split-KV partials: out = sum_s w_s O_s / sum_s w_s with
-// w_s = 2^(lse_s - max lse).  One thread per 4 output channels of one
-// (layer, sequence, query, head); rows that no sequence owns (outside every
-// cu_q range) are left untouched, as the one-pass kernels leave them.
-__global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
+// w_s = 2^(lse_s - max lse).  Grid (row tiles, sequences from seq0, layers);
+// a thread takes kCombineCV 16-byte chunks of one (query, head) output row,
+// so its index arithmetic (32-bit) and log-sum-exp loads serve several
+// chunks.  Rows that no sequence owns (outside every cu_q range) are left
+// untouched, as the one-pass kernels leave them.
+constexpr int kCombineCV = 2;   // 16-byte output chunks per thread
+constexpr int kCombineCB = 8;   // splits whose partials are loaded in one batch
+__global__ __launch_bounds__(256) void attn_combine(AttnArgs a, int seq0) {
+    constexpr int CV = kCombineCV, CB = kCombineCB;
     const int dv = a.head_dim_v;
-    const int chunks = dv / 4;
     const int64_t items = (int64_t)a.n_layers * a.total_q * a.n_heads;   // partial records per split
-    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t slot = gid / chunks;    // (layer, sequence, query of the sequence, head)
-    const int c = (int)(gid % chunks);
-    if (slot >= (int64_t)a.n_layers * a.n_seqs * a.max_q * a.n_heads) return;
-    const int head = (int)(slot % a.n_heads);
-    int64_t rest = slot / a.n_heads;
-    const int qi = (int)(rest % a.max_q);
-    rest /= a.max_q;
-    const int seq = (int)(rest % a.n_seqs);
-    const int layer = (int)(rest / a.n_seqs);
+    const uint32_t per_item = (uint32_t)dv / (4 * CV);                  // threads per (query, head)
+    const uint32_t idx = blockIdx.x * 256u + threadIdx.x;
+    const uint32_t rh = idx / per_item;
+    const int c0 = (int)(idx - rh * per_item) * CV;                      // first chunk of this thread
+    const uint32_t qi = rh / (uint32_t)a.n_heads;
+    const int head = (int)(rh - qi * (uint32_t)a.n_heads);
+    if (qi >= (uint32_t)a.max_q) return;
+    const int seq = seq0 + (int)blockIdx.y;
+    const int layer = (int)blockIdx.z;
     int q0 = 0, nq = a.total_q;
     if (a.cu_q) {
         q0 = a.cu_q[seq];
         nq = a.cu_q[seq + 1] - q0;
     }
     if (q0 < 0 || nq < 0 || (int64_t)q0 + nq > a.total_q) nq = 0;   // as seq_info
-    if (qi >= nq) return;
-    const int64_t row = q0 + qi;
+    if ((int)qi >= nq) return;
+    const int64_t row = q0 + (int)qi;
     const int64_t item = ((int64_t)layer * a.total_q + row) * a.n_heads + head;
     // The log-sum-exps and partial outputs of up to CB splits are loaded in
     // one batch (independent loads: one memory round trip), then weighted by
     // w_s = 2^(lse_s - max) and summed in split order; a later batch (more
     // than CB splits) rescales the sums to its larger maximum.
-    constexpr int CB = 16;
     const int ns = a.n_splits;
     float mx = -INFINITY, wsum = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    f32x4 acc[CV];
+#pragma unroll
+    for (int k = 0; k < CV; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int s0 = 0; s0 < ns; s0 += CB) {
         float l[CB];
-        f32x4 v[CB];
+        f32x4 v[CB][CV];
 #pragma unroll
         for (int j = 0; j < CB; ++j) {
             const bool in = s0 + j < ns;
             l[j] = in ? a.ws_lse[(int64_t)(s0 + j) * items + item] : -INFINITY;
-            v[j] = in ? *(const f32x4*)(a.ws_o + ((int64_t)(s0 + j) * items + item) * dv + c * 4)
-                      : f32x4{0.f, 0.f, 0.f, 0.f};
+            const float* src = a.ws_o + ((int64_t)(s0 + j) * items + item) * dv + c0 * 4;
+#pragma unroll
+            for (int k = 0; k < CV; ++k) v[j][k] = in ? *(const f32x4*)(src + k * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
         }
         float bm = -INFINITY;
 #pragma unroll
@@ -227,7 +232,8 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
         if (bm > mx) {
             if (mx != -INFINITY) {
                 const float r = __builtin_amdgcn_exp2f(mx - bm);
-                acc *= r;
+#pragma unroll
+                for (int k = 0; k < CV; ++k) acc[k] *= r;
                 wsum *= r;
             }
             mx = bm;
@@ -236,21 +242,26 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
         for (int j = 0; j < CB; ++j) {
             if (l[j] == -INFINITY) continue;
             const float w = __builtin_amdgcn_exp2f(l[j] - mx);
-            acc += w * v[j];
+#pragma unroll
+            for (int k = 0; k < CV; ++k) acc[k] += w * v[j][k];
             wsum += w;
         }
     }
     const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-    const int64_t oofs = (int64_t)layer * a.o_stride[0] + row * a.o_stride[1] + (int64_t)head * a.o_stride[2] + c * 4;
-    if (a.dtype == 1) {
-        *(f32x4*)((float*)a.out + oofs) = f32x4{acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv};
-    } else {
-        u32x2 w;
-        w[0] = bf_rne(acc[0] * inv) | (bf_rne(acc[1] * inv) << 16);
-        w[1] = bf_rne(acc[2] * inv) | (bf_rne(acc[3] * inv) << 16);
-        *(u32x2*)((uint16_t*)a.out + oofs) = w;
+    const int64_t oofs = (int64_t)layer * a.o_stride[0] + row * a.o_stride[1] + (int64_t)head * a.o_stride[2] + c0 * 4;
+#pragma unroll
+    for (int k = 0; k < CV; ++k) {
+        if (a.dtype == 1) {
+            *(f32x4*)((float*)a.out + oofs + k * 4) =
+                f32x4{acc[k][0] * inv, acc[k][1] * inv, acc[k][2] * inv, acc[k][3] * inv};
+        } else {
+            u32x2 w;
+            w[0] = bf_rne(acc[k][0] * inv) | (bf_rne(acc[k][1] * inv) << 16);
+            w[1] = bf_rne(acc[k][2] * inv) | (bf_rne(acc[k][3] * inv) << 16);
+            *(u32x2*)((uint16_t*)a.out + oofs + k * 4) = w;
+        }
     }
-    if (a.lse_out && c == 0)
+    if (a.lse_out && c0 == 0)
         a.lse_out[item] = wsum > 0.f ? (mx + __log2f(wsum)) * kLn2 : -INFINITY;
 }
 
@@ -363,11 +374,18 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
         e = a.variant == 1 ? launch_attn_mla_bf16(a, p, grid, stream) : launch_attn_gqa_bf16(a, p, grid, stream);
     }
     if (e != hipSuccess || p.splits == 1) return e;
-    const int64_t threads = (int64_t)a.n_layers * a.n_seqs * a.max_q * a.n_heads * (a.head_dim_v / 4);
-    if (threads == 0) return hipSuccess;
-    dim3 cgrid((unsigned)((threads + 255) / 256));
-    hipLaunchKernelGGL(attn_combine, cgrid, block, 0, stream, a);
-    return hipGetLastError();
+    // One (row tiles, sequences, layers) grid per 65535 sequences.
+    const int64_t threads = (int64_t)a.max_q * a.n_heads * (a.head_dim_v / (4 * kCombineCV));
+    if (threads == 0 || a.n_layers == 0 || a.n_seqs == 0) return hipSuccess;
+    if (a.head_dim_v % (4 * kCombineCV) || threads > 0xffffffffLL || a.n_layers > 65535) return hipErrorInvalidValue;
+    for (int seq0 = 0; seq0 < a.n_seqs; seq0 += 65535) {
+        const int nseq = a.n_seqs - seq0 < 65535 ? a.n_seqs - seq0 : 65535;
+        dim3 cgrid((unsigned)((threads + 255) / 256), (unsigned)nseq, (unsigned)a.n_layers);
+        hipLaunchKernelGGL(attn_combine, cgrid, block, 0, stream, a, seq0);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace pkv
