@@ -52,7 +52,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kUnroll = 1;         // rows whose loads are issued before any is used
 constexpr int kRowsPerBlock = 1;   // (layer, kv_head) rows per block
 constexpr int kBlock = 256;        // threads per block
-constexpr int kSegTiles = 8;       // segment mode: token-tile blocks per (row group, segment)
+constexpr int kSegTiles = 32;      // segment mode: token-tile blocks per (row group, segment)
 constexpr int kSegAhead = 6;       // segment mode: tiles whose loads are issued before the first store
 constexpr int kHalf = 0;
 constexpr int kWave = 64;
@@ -218,18 +218,20 @@ __global__ __launch_bounds__(kBlock) void splice_kernel(SpliceArgs a, Geo g, Fre
     // segments that read the same source chunk (a shared skill) find it in the
     // caches.  When the row groups divide evenly over the XCDs, segment mode
     // runs on a 1-D grid whose ids are dealt to the XCDs round-robin: XCD x
-    // takes row groups x*seg_xcd_rows .. and, within them, the same
-    // (segment fastest) order, so every read of one source chunk goes through
-    // one XCD's L2 and only the first reaches memory.
+    // takes row groups x*seg_xcd_rows .. one at a time, so every read of one
+    // source chunk goes through one XCD's L2 and only the first reaches
+    // memory; within a row the tile blocks of one segment are consecutive, so
+    // the blocks in flight write into few destination ranges (a row's source
+    // chunks, a few MB, stay in that L2 meanwhile).
     int grp = blockIdx.y, seg_i = 0, tile_blk = 0, tile_blocks = 1;
     if constexpr (SEG) {
         if (g.seg_xcd_rows) {
             const uint32_t id = blockIdx.x;
             const uint32_t slot = id / kXcds;
-            seg_i = (int)(slot % (uint32_t)g.seg_n);
-            const uint32_t rest = slot / (uint32_t)g.seg_n;
-            tile_blk = (int)(rest % (uint32_t)g.seg_tile_blocks);
-            grp = (int)(id % kXcds) * g.seg_xcd_rows + (int)(rest / (uint32_t)g.seg_tile_blocks);
+            tile_blk = (int)(slot % (uint32_t)g.seg_tile_blocks);
+            const uint32_t rest = slot / (uint32_t)g.seg_tile_blocks;
+            seg_i = (int)(rest % (uint32_t)g.seg_n);
+            grp = (int)(id % kXcds) * g.seg_xcd_rows + (int)(rest / (uint32_t)g.seg_n);
             tile_blocks = g.seg_tile_blocks;
         } else {
             seg_i = blockIdx.x;
