@@ -212,3 +212,27 @@ def test_mla_score_spike_reruns_the_key_range():
         want, _ = oracle.attention(qh[0], rh[0], rh[0][..., :512], q_pos, kv, scale)
         log("  spike splits %d" % splits, check_attention_close(got[0], want))
         np.testing.assert_allclose(bits_to_f64(got[0, 5, 7]), bits_to_f64(rh[0, 0, 700, :512]), atol=3e-2)
+
+
+def test_more_sequences_than_one_combine_grid():
+    """65,537 one-query sequences split over the keys: the split merge runs as two grids (at most
+    65,535 sequences each); sequences on both sides of the boundary match the oracle."""
+    n_seqs, kv, H, Hkv, d = 65537, 128, 2, 1, 64
+    g = synth.Draws(61, "cuda")
+    k = g.normal((1, Hkv, n_seqs * kv, d))
+    v = g.normal((1, Hkv, n_seqs * kv, d))
+    q = g.normal((1, n_seqs, H, d))
+    out = torch.zeros(1, n_seqs, H, d, dtype=torch.bfloat16, device="cuda")
+    q_pos = torch.full((n_seqs,), kv - 1, dtype=torch.int32, device="cuda")
+    kv_len = torch.full((n_seqs,), kv, dtype=torch.int32, device="cuda")
+    cu = torch.arange(n_seqs + 1, dtype=torch.int32, device="cuda")
+    base = torch.arange(n_seqs, dtype=torch.int64, device="cuda") * kv
+    log("65537 sequences, 2 splits")
+    pkv.suffix_attention(q, k, v, out, q_pos, kv_len, d ** -0.5, max_kv_len=kv, n_seqs=n_seqs, cu_q=cu,
+                         kv_base=base, max_q=1, n_splits=2)
+    torch.cuda.synchronize()
+    for s in (0, 1, 65534, 65535, 65536):
+        ks = slice(s * kv, (s + 1) * kv)
+        want, _ = oracle.attention(host_bits(q[0, s: s + 1]), host_bits(k[0, :, ks]), host_bits(v[0, :, ks]),
+                                   np.array([kv - 1], dtype=np.int32), kv, d ** -0.5)
+        check_attention_close(host_bits(out[0, s: s + 1]), want)
