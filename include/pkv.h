@@ -8,13 +8,14 @@
  *   - Sec. 5 ("From mechanism to prediction") and Fig. "Two cache operations"
  *     (b): a chunk's KV is computed once at source positions; because the
  *     cache stores post-RoPE keys, moving it re-rotates every key from its
- *     source position to its target position, values are position-free, and
+ *     source position to its target position, values carry no position, and
  *     the result is spliced into the destination cache without a reprefill.
  *     App. B's skill example fixes the source positions 0..L-1 and a target
  *     offset.
  *   - Sec. 8 (MLA adapter) and Fig. "attention-variant adapters" (a): an MLA
- *     cache row holds a position-free latent plus a small decoupled-RoPE k_pe
- *     slice; repositioning rotates only k_pe and copies the latent as-is.
+ *     cache row holds a latent part with no rotary position and a 64-channel
+ *     k_pe part that is rotated; repositioning rotates only k_pe and copies the
+ *     latent as-is.
  *   - Sec. 5 ("Linear-time TTFT"): the transplant costs a re-rotation pass plus
  *     the suffix; the suffix (or an appended erratum, Sec. 4) attends causally
  *     over the spliced cache.
@@ -176,8 +177,8 @@ typedef struct pkv_paged_cache {
     int64_t page_stride_k;       /* elements between consecutive physical pages of K */
     int64_t page_stride_v;       /* ... of V (unused when there is no V tensor) */
     const int32_t* v_block_table;  /* optional device int32 [n_seqs][max_pages]: V pages through
-                                      their own table (NULL: block_table for both).  Values are
-                                      position-free, so a spliced chunk's value pages can be
+                                      their own table (NULL: block_table for both).  Values carry
+                                      no position, so a spliced chunk's value pages can be
                                       referenced in place instead of copied (GQA only). */
 } pkv_paged_cache;
 

@@ -27,7 +27,7 @@
  *     cache operations" (b); App. B skill example): the cached keys are
  *     post-RoPE, so a chunk cached at source positions is moved to target
  *     positions by rotating each key by delta = dst_pos - src_pos and writing it
- *     to the destination slot dst_pos; values are position-free and are copied
+ *     to the destination slot dst_pos; values carry no position and are copied
  *     unchanged.  MLA adapter (Sec. 8 and Fig. "attention-variant adapters"
  *     (a)): only the decoupled k_pe slice rotates, the latent is copied as-is.
  *   - Causal attention of the suffix/erratum queries over the spliced cache

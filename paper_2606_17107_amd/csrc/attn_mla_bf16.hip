@@ -1,8 +1,8 @@
 // bf16 MLA suffix attention (absorbed form) for gfx950.
 //
 // The MLA cache keeps, per token, one latent row [c_kv (512) | k_pe (64)]
-// shared by every head (paper Sec. 8, MLA adapter: the latent is position-free
-// and only the small decoupled-RoPE slice carries positions).  With absorbed
+// shared by every head (paper Sec. 8, MLA adapter: no rotation is applied to
+// c_kv; only the 64 k_pe channels are rotated by position).  With absorbed
 // queries q = [q_latent (512) | q_pe (64)] per head, the scores run over all
 // 576 channels and the values are the 512 latent channels of the same row:
 //     o_h = sum_j softmax_j(scale <q_h, row_j>) row_j[0:512]
