@@ -317,7 +317,7 @@ int attention_splits(const AttnArgs& a) {
     // for its start-up, first loads and partial write, plus 1/s of the keys),
     // plus, for s > 1, the split partials written and read back by the
     // combine pass.  Nominal rates (measured on MI355X): the bf16 kernels
-    // sustain about 1.0 PFLOP/s (GQA) and 0.75 PFLOP/s (MLA), a workgroup's
+    // sustain about 1.0 PFLOP/s (GQA) and 1.1 PFLOP/s (MLA), a workgroup's
     // fixed cost is about 20 us, the combine streams at about 5 TB/s.  At
     // least 512 keys per split, at most 32 splits.
     const Plan p = make_plan(a, 1);
@@ -332,7 +332,7 @@ int attention_splits(const AttnArgs& a) {
         return s < 1 ? 1 : (int)s;
     }
     const int64_t slots = kCUs * (int64_t)wgs_per_cu(a, p);
-    const double rate = a.variant == 1 ? 0.75e15 : 1.0e15;
+    const double rate = a.variant == 1 ? 1.1e15 : 1.0e15;
     const double slot_rate = rate / (double)slots;
     const double wg_flops = (double)p.BM * a.max_kv_len * (a.head_dim + a.head_dim_v) * 2.0;
     const double comb_bytes = (double)a.n_layers * a.total_q * a.n_heads * (a.head_dim_v + 1) * 4.0 * 2.0;
