@@ -261,9 +261,9 @@ typedef struct pkv_attn_desc {
     const int32_t* cu_q;    /* device int32 [n_seqs+1]; NULL allowed when n_seqs == 1 */
     const int64_t* kv_base; /* device int64 [n_seqs]; NULL = every sequence starts at slot 0 */
     int64_t cache_slots;    /* slots present in k_cache/v_cache; reads past it are masked out */
-    int64_t q_stride[3];
-    int64_t k_stride[3];
-    int64_t v_stride[3];
+    int64_t q_stride[3];    /* every stride in elements, non-negative, a multiple of 16 bytes */
+    int64_t k_stride[3];    /* the slot strides k_stride[2] and v_stride[2] at most 64 MiB (the */
+    int64_t v_stride[3];    /* kernels address the keys of one tile by 32-bit byte offsets) */
     int64_t o_stride[3];
     float* lse_out;         /* optional device fp32 [n_layers][total_q][n_q_heads]: natural-log
                                log-sum-exp of the visible scaled scores (-inf for an empty row) */

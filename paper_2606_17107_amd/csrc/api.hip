@@ -252,6 +252,12 @@ pkv_status check_attention(const void* q, const void* k, const void* v, void* ou
             (d->o_stride[i] * eb) % 16)
             return fail(PKV_ERR_ALIGN, "strides must be multiples of 16 bytes");
     }
+    // The kernels address the keys of one tile (up to 32 slots) by 32-bit byte
+    // offsets from its first key.
+    constexpr int64_t kMaxSlotBytes = (int64_t)1 << 26;
+    if (d->k_stride[2] > kMaxSlotBytes / eb || d->v_stride[2] > kMaxSlotBytes / eb)
+        return fail(PKV_ERR_SHAPE, "slot strides k_stride[2] / v_stride[2] (%lld / %lld elements) exceed 64 MiB",
+                    (long long)d->k_stride[2], (long long)d->v_stride[2]);
     int page_shift = 0;
     if (pg) {
         if (d->dtype != PKV_BF16) return fail(PKV_ERR_UNSUPPORTED, "paged attention is bf16 only");

@@ -158,6 +158,11 @@ def attend(d, H=32, Hkv=8, D=128, q=Q, k=K, v=V, o=O, qp=QP, kl=KL, ws=None, wsb
     (dict(q_stride=pkv._i64x3(64 * 32 * 128, 32 * 128, 100)), {}, pkv.PKV_ERR_ALIGN),
     ({}, dict(o=K + 4096), pkv.PKV_ERR_ALIAS),
     ({}, dict(scale=float("nan")), pkv.PKV_ERR_SHAPE),
+    # slot strides above 64 MiB (a tile's keys are addressed by 32-bit offsets); exactly 64 MiB passes
+    # that check and fails the later alias check instead
+    (dict(k_stride=pkv._i64x3(8 * 1000 * 128, 1000 * 128, (1 << 25) + 8)), {}, pkv.PKV_ERR_SHAPE),
+    (dict(v_stride=pkv._i64x3(8 * 1000 * 128, 1000 * 128, (1 << 25) + 8)), {}, pkv.PKV_ERR_SHAPE),
+    (dict(k_stride=pkv._i64x3(8 * 1000 * 128, 1000 * 128, 1 << 25)), dict(o=K + 4096), pkv.PKV_ERR_ALIAS),
 ])
 def test_attention_validation(kw, args, want):
     st = attend(attn_desc(**kw), **args)
