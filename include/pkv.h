@@ -252,7 +252,7 @@ typedef struct pkv_attn_desc {
     int32_t head_dim_v;     /* == head_dim for GQA; 512 for MLA */
     int32_t total_q;        /* query rows per layer over all sequences */
     int32_t max_q;          /* >= the largest per-sequence query count */
-    int32_t max_kv_len;     /* >= every kv_len[s]; larger values are clamped to it */
+    int32_t max_kv_len;     /* >= every kv_len[s]; larger values are clamped to it; at most 2^30 */
     int32_t n_splits;       /* KV-length splits; 0 = the library chooses (at most 32); an explicit
                                count above ceil(max_kv_len / 64) is lowered to it */
     int32_t window;         /* 0: full causal attention.  W > 0: sliding window, slot j is visible
@@ -291,8 +291,8 @@ size_t pkv_attention_workspace_size(const pkv_attn_desc* desc, int32_t n_q_heads
  * pkv_attention_workspace_size() bytes (may be NULL when that is 0), owned by
  * the caller, contents scratch.
  * Errors: PKV_ERR_NULL, PKV_ERR_SHAPE (n_q_heads % n_kv_heads != 0, sizes <= 0,
- * window < 0, workspace too small, MLA shape not 576/512 with one KV head or v_cache not
- * k_cache), PKV_ERR_ALIGN,
+ * max_kv_len > 2^30, slot strides above 64 MiB, window < 0, workspace too small,
+ * MLA shape not 576/512 with one KV head or v_cache not k_cache), PKV_ERR_ALIGN,
  * PKV_ERR_UNSUPPORTED (head_dim other than 64 or 128 for GQA; fp32 MLA),
  * PKV_ERR_DEVICE. */
 pkv_status pkv_suffix_attention(const void* q, const void* k_cache, const void* v_cache, void* out,

@@ -227,6 +227,8 @@ pkv_status check_attention(const void* q, const void* k, const void* v, void* ou
     if (d->n_layers <= 0 || d->n_seqs <= 0 || d->total_q < 0 || d->max_q < 0 || d->max_kv_len < 0 ||
         d->n_splits < 0 || d->cache_slots < 0 || d->head_dim_v <= 0)
         return fail(PKV_ERR_SHAPE, "invalid sizes in desc");
+    if (d->max_kv_len > (1 << 30))   // key indices and tile arithmetic stay inside int32
+        return fail(PKV_ERR_SHAPE, "max_kv_len (%d) above 2^30", d->max_kv_len);
     if (d->n_seqs > 1 && !d->cu_q) return fail(PKV_ERR_NULL, "cu_q is required when n_seqs > 1");
     if (d->n_seqs == 1 && !d->cu_q && d->max_q < d->total_q)
         return fail(PKV_ERR_SHAPE, "max_q (%d) < total_q (%d)", d->max_q, d->total_q);

@@ -43,8 +43,8 @@ __global__ __launch_bounds__(256) void attn_gqa_f32(AttnArgs a, Plan p) {
     const int qi = row_ok ? m / p.G : 0;
     const int head = kvh * p.G + (row_ok ? m - qi * p.G : 0);
     const int qpos = row_ok ? a.q_pos[si.q0 + qi] : -1;
-    const int row_end = row_ok ? max(0, min(si.kvl, qpos + 1)) : 0;
-    const int row_start = a.window > 0 && row_ok ? max(0, qpos - a.window + 1) : 0;   // sliding window
+    int row_start, row_end;
+    visible_range(qpos, si.kvl, a.window, row_start, row_end);   // (0, 0) for rows past M
     const int wmax = wave_max_i(row_end);
     const int wsmin = wave_min_i(row_ok ? row_start : 0x7fffffff);
     if ((tid & 63) == 0) {

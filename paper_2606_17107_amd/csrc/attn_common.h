@@ -123,6 +123,16 @@ struct PageWindow {
     }
 };
 
+// Visible keys [start, end) of a row at position qpos over a cache of kvl
+// keys: causal (keys up to qpos) and, with a window W > 0, keys above
+// qpos - W.  Both bounds lie in [0, kvl] and are formed without overflow for
+// every int32 position and window; a row before the cache (qpos < 0) sees
+// nothing.
+__device__ inline void visible_range(int qpos, int kvl, int window, int& start, int& end) {
+    end = qpos < kvl ? max(0, qpos + 1) : kvl;
+    start = window > 0 && qpos >= window ? min(qpos - window + 1, kvl) : 0;
+}
+
 __device__ inline int wave_max_i(int v) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) v = max(v, __shfl_xor(v, o));

@@ -129,8 +129,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_gqa_bf16_kernel(AttnArgs 
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
         const int qpos = row_ok[qb] ? a.q_pos[si.q0 + qi[qb]] : -1;
-        row_end[qb] = row_ok[qb] ? max(0, min(si.kvl, qpos + 1)) : 0;
-        row_start[qb] = a.window > 0 && row_ok[qb] ? max(0, qpos - a.window + 1) : 0;
+        visible_range(qpos, si.kvl, a.window, row_start[qb], row_end[qb]);   // (0, 0) for rows past M
         rmax = max(rmax, row_end[qb]);
         if (row_ok[qb]) {
             rmin = min(rmin, row_end[qb]);

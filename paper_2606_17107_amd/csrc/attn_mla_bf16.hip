@@ -121,8 +121,8 @@ __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnAr
     const int qpos = row_ok ? a.q_pos[si.q0 + qi] : -1;
     // Visible keys [row_start, row_end): causal, and with a sliding window
     // also row_start = q_pos - window + 1.
-    const int row_end = row_ok ? max(0, min(si.kvl, qpos + 1)) : 0;
-    const int row_start = a.window > 0 && row_ok ? max(0, qpos - a.window + 1) : 0;
+    int row_start, row_end;
+    visible_range(qpos, si.kvl, a.window, row_start, row_end);   // (0, 0) for rows past M
     const int wmin = wave_min_i(row_ok ? row_end : 0x7fffffff);
     const int wmax = wave_max_i(row_end);
     const int wsmin = wave_min_i(row_ok ? row_start : 0x7fffffff);

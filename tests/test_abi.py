@@ -163,6 +163,8 @@ def attend(d, H=32, Hkv=8, D=128, q=Q, k=K, v=V, o=O, qp=QP, kl=KL, ws=None, wsb
     (dict(k_stride=pkv._i64x3(8 * 1000 * 128, 1000 * 128, (1 << 25) + 8)), {}, pkv.PKV_ERR_SHAPE),
     (dict(v_stride=pkv._i64x3(8 * 1000 * 128, 1000 * 128, (1 << 25) + 8)), {}, pkv.PKV_ERR_SHAPE),
     (dict(k_stride=pkv._i64x3(8 * 1000 * 128, 1000 * 128, 1 << 25)), dict(o=K + 4096), pkv.PKV_ERR_ALIAS),
+    (dict(max_kv_len=(1 << 30) + 1), {}, pkv.PKV_ERR_SHAPE),       # key arithmetic stays inside int32
+    (dict(max_kv_len=1 << 30), dict(o=K + 4096), pkv.PKV_ERR_ALIAS),
 ])
 def test_attention_validation(kw, args, want):
     st = attend(attn_desc(**kw), **args)

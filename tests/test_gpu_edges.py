@@ -236,3 +236,51 @@ def test_more_sequences_than_one_combine_grid():
         want, _ = oracle.attention(host_bits(q[0, s: s + 1]), host_bits(k[0, :, ks]), host_bits(v[0, :, ks]),
                                    np.array([kv - 1], dtype=np.int32), kv, d ** -0.5)
         check_attention_close(host_bits(out[0, s: s + 1]), want)
+
+
+EXTREME_POS = np.array([2 ** 31 - 1, 2 ** 31 - 40, -2 ** 31, -1, 0, 1, 31, 32, 299, 300, 301, 5000], np.int32)
+
+
+@pytest.mark.parametrize("variant,dtype,d,window", [
+    ("gqa", "bf16", 128, 0), ("gqa", "bf16", 128, 1), ("gqa", "bf16", 64, 37), ("gqa", "bf16", 128, 2 ** 31 - 1),
+    ("gqa", "f32", 64, 0), ("gqa", "f32", 128, 37), ("mla", "bf16", 576, 0), ("mla", "bf16", 576, 2 ** 31 - 40)])
+def test_extreme_positions(variant, dtype, d, window):
+    """Query positions at both ends of the int32 range (far past the cache, before it) and windows up
+    to 2^31 - 1: each row sees exactly the slots the contract names (j < kv_len, j <= q_pos,
+    j > q_pos - window), in one pass and split, against the oracle.  (The oracle forms the bounds in
+    64-bit integers; q_pos + 1 and q_pos - window + 1 overflow int32 at these values.)"""
+    L, kv, n_q = 1, 300, EXTREME_POS.size
+    H, Hkv = (16, 1) if variant == "mla" else (8, 2)
+    dv = 512 if variant == "mla" else d
+    g = synth.Draws(43 + d + (window % 1000), "cpu")
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    q = g.normal((L, n_q, H, d), tdt)
+    k = g.normal((L, Hkv, kv + 4, d), tdt)
+    v = k[..., :512] if variant == "mla" else g.normal((L, Hkv, kv + 4, d), tdt)
+    scale = 1 / np.sqrt(192.0 if variant == "mla" else d)
+    host = (lambda t: t.numpy().astype(np.float64)) if dtype == "f32" else host_bits
+    qh, kh = host(q), host(k)
+    vh = kh[..., :512] if variant == "mla" else host(v)
+    for splits in (1, 3):
+        out = torch.zeros(L, n_q, H, dv, dtype=tdt, device="cuda")
+        lse = torch.zeros(L, n_q, H, dtype=torch.float32, device="cuda")
+        kd = k.cuda()
+        vd = kd[..., :512] if variant == "mla" else v.cuda()
+        log("extreme positions: %s %s d %d window %d splits %d" % (variant, dtype, d, window, splits))
+        pkv.suffix_attention(q.cuda(), kd, vd, out, torch.from_numpy(EXTREME_POS).cuda(),
+                             torch.tensor([kv], dtype=torch.int32, device="cuda"), scale, max_kv_len=kv,
+                             variant=pkv.PKV_ATTN_MLA if variant == "mla" else pkv.PKV_ATTN_GQA, n_splits=splits,
+                             lse_out=lse, window=window)
+        torch.cuda.synchronize()
+        if dtype == "f32":
+            want, want_lse = oracle.attention(q[0].numpy(), k[0].numpy(), v[0].contiguous().numpy(), EXTREME_POS, kv,
+                                              scale, window=window)
+            assert np.abs(out[0].cpu().numpy() - want).max() <= 1e-5
+        else:
+            want, want_lse = oracle.attention(qh[0], kh[0], np.ascontiguousarray(vh[0]), EXTREME_POS, kv, scale,
+                                              window=window)
+            check_attention_close(host_bits(out)[0], want)
+        got_lse = lse[0].cpu().numpy()
+        empty = np.isneginf(want_lse)
+        assert np.array_equal(np.isneginf(got_lse), empty)
+        np.testing.assert_allclose(got_lse[~empty], want_lse[~empty], rtol=1e-4, atol=1e-4)
