@@ -162,6 +162,63 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream
 
 
+# ---- argument checks of the tensor-level calls --------------------------------
+# The C entry points take raw device addresses; a host tensor's address handed
+# to a kernel would fault the GPU.  The tensor-level calls below check type,
+# dtype, size and device of every tensor they pass down (the raw pkv_* calls
+# above do not).
+
+def _need(t, name: str, device: torch.device, dtype=None, numel: Optional[int] = None,
+          contiguous: bool = False) -> None:
+    if t is None:
+        return
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor, got %s" % (name, type(t).__name__))
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if numel is not None and t.numel() < numel:
+        raise ValueError("%s holds %d elements, the call reads %d" % (name, t.numel(), numel))
+    if contiguous and not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if t.device != device:
+        raise ValueError("%s is on %s, the call runs on %s" % (name, t.device, device))
+
+
+def _gpu_device(t: torch.Tensor, name: str) -> torch.device:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor, got %s" % (name, type(t).__name__))
+    if t.device.type != "cuda":
+        raise ValueError("libpkv tensors live on the GPU: %s is on %s" % (name, t.device))
+    return t.device
+
+
+def _check_splice_args(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, err_flag, dst_slot=None,
+                       n_tokens: Optional[int] = None) -> None:
+    dev = _gpu_device(src_k, "src_k")
+    n = src_k.shape[2] if n_tokens is None else n_tokens
+    for t, name in ((src_v, "src_v"), (dst_k, "dst_k"), (dst_v, "dst_v")):
+        _need(t, name, dev, src_k.dtype)
+    for t, name in ((src_pos, "src_pos"), (dst_pos, "dst_pos"), (dst_slot, "dst_slot")):
+        _need(t, name, dev, torch.int32, n, contiguous=True)
+    _need(err_flag, "err_flag", dev, torch.int32, 1)
+
+
+def _check_attention_args(q, k_cache, v_cache, out, q_pos, kv_len, n_seqs, cu_q, kv_base, lse_out,
+                          workspace) -> None:
+    dev = _gpu_device(q, "q")
+    for t, name in ((k_cache, "k_cache"), (v_cache, "v_cache"), (out, "out")):
+        if t is None:
+            raise TypeError("%s is required" % name)
+        _need(t, name, dev, q.dtype)
+    L, rows, H = q.shape[0], q.shape[1], q.shape[2]
+    _need(q_pos, "q_pos", dev, torch.int32, rows, contiguous=True)
+    _need(kv_len, "kv_len", dev, torch.int32, int(n_seqs), contiguous=True)
+    _need(cu_q, "cu_q", dev, torch.int32, int(n_seqs) + 1, contiguous=True)
+    _need(kv_base, "kv_base", dev, torch.int64, int(n_seqs), contiguous=True)
+    _need(lse_out, "lse_out", dev, torch.float32, L * rows * H, contiguous=True)
+    _need(workspace, "workspace", dev, contiguous=True)
+
+
 # ---- raw C entry points (same names and arguments as pkv.h) -----------------
 
 def pkv_reposition_splice(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, rope_theta, rope_dim, layout,
@@ -277,6 +334,7 @@ def make_layout(src_k: torch.Tensor, src_v: Optional[torch.Tensor], dst_k: torch
 def reposition_splice(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, rope_theta, rope_dim, rope_offset=0,
                       rope_style=PKV_ROPE_HALF, err_flag=None, stream=None) -> None:
     """Tensor-level call of pkv_reposition_splice; raises PkvError on a non-OK status."""
+    _check_splice_args(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, err_flag)
     layout = make_layout(src_k, src_v, dst_k, dst_v, rope_offset, rope_style, err_flag=err_flag)
     _check(pkv_reposition_splice(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, rope_theta, rope_dim, layout,
                                  stream))
@@ -286,6 +344,7 @@ def reposition_splice_freqs(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, omega,
                             rope_style=PKV_ROPE_HALF, dst_slot=None, err_flag=None, stream=None) -> None:
     """Tensor-level call of pkv_reposition_splice_freqs (per-pair frequencies ``omega``; optional
     destination slots, else slot = dst_pos)."""
+    _check_splice_args(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, err_flag, dst_slot)
     layout = make_layout(src_k, src_v, dst_k, dst_v, rope_offset, rope_style, err_flag=err_flag)
     _check(pkv_reposition_splice_freqs(src_k, src_v, dst_k, dst_v, src_pos, dst_pos, dst_slot, omega, rope_dim,
                                        layout, stream))
@@ -305,6 +364,9 @@ def make_segments(segs: Sequence[dict], device) -> torch.Tensor:
 def reposition_splice_batched(src_k, src_v, dst_k, dst_v, segs_dev: torch.Tensor, n_segs: int,
                               max_seg_tokens: int, rope_theta, rope_dim, rope_offset=0,
                               rope_style=PKV_ROPE_HALF, err_flag=None, stream=None) -> None:
+    _check_splice_args(src_k, src_v, dst_k, dst_v, None, None, err_flag)
+    _need(segs_dev, "segs_dev", src_k.device, torch.uint8, int(n_segs) * ctypes.sizeof(pkv_segment),
+          contiguous=True)
     layout = make_layout(src_k, src_v, dst_k, dst_v, rope_offset, rope_style, err_flag=err_flag)
     _check(pkv_reposition_splice_batched(src_k, src_v, dst_k, dst_v, segs_dev, n_segs, max_seg_tokens,
                                          rope_theta, rope_dim, layout, stream))
@@ -351,6 +413,7 @@ def suffix_attention(q, k_cache, v_cache, out, q_pos, kv_len, scale, max_kv_len,
                      kv_base=None, max_q=None, variant=PKV_ATTN_GQA, n_splits=0, lse_out=None,
                      workspace=None, stream=None, window=0) -> None:
     """Tensor-level call of pkv_suffix_attention (allocates the workspace with torch if not given)."""
+    _check_attention_args(q, k_cache, v_cache, out, q_pos, kv_len, n_seqs, cu_q, kv_base, lse_out, workspace)
     H = q.shape[2]
     Hkv = k_cache.shape[1]
     D = q.shape[3]
@@ -398,6 +461,9 @@ def reposition_splice_paged(src_k, src_v, k_pool, v_pool, src_pos, dst_pos, bloc
                             stream=None, v_block_table=None) -> None:
     """Tensor-level call of pkv_reposition_splice_paged: destination slots are logical slots of the
     sequence whose block-table row is block_table[0]."""
+    _check_splice_args(src_k, src_v, k_pool, v_pool, src_pos, dst_pos, err_flag)
+    _need(block_table, "block_table", src_k.device, torch.int32, contiguous=True)
+    _need(v_block_table, "v_block_table", src_k.device, torch.int32, contiguous=True)
     L = make_layout(src_k, src_v, src_k, src_v, rope_offset, rope_style, err_flag=err_flag)
     L.dst_capacity = (block_table.shape[1] * k_pool.shape[2]) if dst_capacity is None else int(dst_capacity)
     L.dst_k_stride = pool_strides3(k_pool)
@@ -411,6 +477,9 @@ def suffix_attention_paged(q, k_pool, v_pool, out, q_pos, kv_len, block_table, s
                            cu_q=None, max_q=None, variant=PKV_ATTN_GQA, n_splits=0, lse_out=None, workspace=None,
                            stream=None, window=0, cache_slots=None, v_block_table=None) -> None:
     """Tensor-level call of pkv_suffix_attention_paged (q [L][rows][H][d], pools as above)."""
+    _check_attention_args(q, k_pool, v_pool, out, q_pos, kv_len, n_seqs, cu_q, None, lse_out, workspace)
+    _need(block_table, "block_table", q.device, torch.int32, contiguous=True)
+    _need(v_block_table, "v_block_table", q.device, torch.int32, contiguous=True)
     H = q.shape[2]
     Hkv = k_pool.shape[3]
     D = q.shape[3]
