@@ -307,6 +307,20 @@ def test_mla_small(splits):
         np.testing.assert_allclose(lse[l], wl, atol=2e-2)
 
 
+@pytest.mark.parametrize("H", [8, 128])
+def test_mla_head_counts(H):
+    """Absorbed MLA with 8 heads (a 32-row MFMA block spans four queries) and 128 heads (the
+    DeepSeek-V2 count: one query's rows fill a whole workgroup), one pass and split."""
+    L, n_q, kv = 1, 5, 530
+    q, rows, q_pos = mla_case(L, H, n_q, kv, 10 + H)
+    scale = 1 / math.sqrt(192)
+    for splits in (1, 3):
+        got, lse = gpu_mla(q, rows, q_pos, kv, scale, splits, lse=True)
+        want, wl = oracle.attention(q[0], rows[0], rows[0][..., :512], q_pos, kv, scale)
+        log("  mla H=%d splits=%d" % (H, splits), check_attention_close(got[0], want))
+        np.testing.assert_allclose(lse[0], wl, atol=2e-2)
+
+
 def test_mla_sharpened():
     L, H, n_q, kv = 1, 16, 6, 400
     q, rows, q_pos = mla_case(L, H, n_q, kv, 9)

@@ -57,9 +57,11 @@ def test_mixed_large_deltas():
     splice_case(deltas, d=576, v_dim=0, r=64, offset=512, style=1, theta=1e4, seed=13)
 
 
-@pytest.mark.parametrize("H,Hkv,d", [(4, 4, 128), (16, 2, 128), (8, 8, 64), (16, 2, 64)])
+@pytest.mark.parametrize("H,Hkv,d", [(4, 4, 128), (16, 2, 128), (8, 8, 64), (16, 2, 64), (12, 4, 128), (40, 8, 128),
+                                     (32, 2, 64), (64, 2, 128)])
 def test_group_sizes(H, Hkv, d):
-    """GQA groups of 1 (multi-head attention) and 8 query heads per KV head."""
+    """GQA groups of 1 (multi-head attention), 3 and 5 (a 32-row MFMA block then holds rows of
+    several queries with the group split across blocks), 8, 16 and 32 query heads per KV head."""
     L, n_q, kv = 2, 37, 611
     g = synth.Draws(20 + H + d, "cpu")
     q = host_bits(g.normal((L, n_q, H, d)))
