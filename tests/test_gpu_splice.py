@@ -95,6 +95,10 @@ CASES = [
     dict(d=64, style=0, rope_dim=64, rope_offset=0, skill=77, L=2, Hkv=5, theta=1e4),
     dict(d=128, style=0, rope_dim=64, rope_offset=32, skill=130, L=2, Hkv=3, theta=1e6),
     dict(d=128, style=1, rope_dim=32, rope_offset=96, skill=33, L=4, Hkv=1, theta=1e4),
+    # head size 256: 128 rotary pairs (the most a row may rotate; more pairs than lanes in a wave, so
+    # every wave forms its own coefficients), and a partial interleaved slice
+    dict(d=256, style=0, rope_dim=256, rope_offset=0, skill=70, L=2, Hkv=2, theta=1e4),
+    dict(d=256, style=1, rope_dim=128, rope_offset=64, skill=45, L=2, Hkv=2, theta=1e6),
 ]
 
 
@@ -140,8 +144,9 @@ def test_scattered_positions(style, d, v_dim, rope_dim, rope_offset):
     compare(w, gk, gv, ok, ov)
 
 
-def test_scattered_positions_fp32():
-    n, cap, L, Hkv, d = 200, 700, 1, 2, 64
+@pytest.mark.parametrize("d", [64, 256])
+def test_scattered_positions_fp32(d):
+    n, cap, L, Hkv = 200, 700, 1, 2
     rng = np.random.default_rng(5)
     g = synth.Draws(13, "cpu")
     skill_k = g.normal((L, Hkv, n, d), torch.float32).numpy()
