@@ -13,15 +13,27 @@ namespace {
 
 constexpr int kCUs = 256;   // compute units of an MI355X
 
-// fp32 GQA kernel: four lanes per row, each holding D/4 channels of q and o;
-// K/V tiles of 32 keys staged in LDS; fp32 online softmax, one step per tile.
+// fp32 GQA kernel on fp32 matrix cores (v_mfma_f32_32x32x2_f32).  Each of the
+// two waves owns 32 rows (query, head-in-group) of one KV head.  As in the
+// bf16 kernel the scores are formed transposed, S^T = K Q^T, so a lane holds 16
+// keys of one row and its probabilities are already the B operand of
+// O^T = V^T P^T: a 2-key step pairs key 8jj + rr (held by lanes 0-31) with key
+// 8jj + 4 + rr (lanes 32-63), both in accumulator register 4jj + rr.  K/V tiles
+// of 32 keys move through registers into LDS (the next tile's loads are in
+// flight while one is consumed): K transposed ([channel][key], a half-wave's 32
+// reads of one score step are 32 consecutive words), V row-major ([key][channel],
+// likewise for the PV operand).  fp32 online softmax with an exact rescale per
+// tile, in log2 units.
 template <int D>
-__global__ __launch_bounds__(256) void attn_gqa_f32(AttnArgs a, Plan p) {
-    constexpr int BN = 32;
-    constexpr int DQ = D / 4;
-    __shared__ float k_lds[BN * D];
-    __shared__ float v_lds[BN * D];
-    __shared__ int red[4], red_start[4];
+__global__ __launch_bounds__(128) void attn_gqa_f32(AttnArgs a, Plan p) {
+    constexpr int BN = 32;                 // keys per tile
+    constexpr int NW = 2;                  // waves, 32 rows each
+    constexpr int KSF = D / 2;             // score steps (2 channels each)
+    constexpr int DB = D / 32;             // 32-channel output blocks
+    constexpr int NL = BN * D / 4 / (NW * 64);   // 16-byte loads per thread per tensor and tile
+    __shared__ __attribute__((aligned(16))) float kt_lds[D * BN];   // [channel][key]
+    __shared__ __attribute__((aligned(16))) float v_lds[BN * D];    // [key][channel]
+    __shared__ int red[NW], red_min[NW], red_start[NW], red_smax[NW];
 
     int group, rb;
     if (!decode(p, group, rb)) return;
@@ -33,146 +45,151 @@ __global__ __launch_bounds__(256) void attn_gqa_f32(AttnArgs a, Plan p) {
     const int seq = rest / a.n_layers;
     const SeqInfo si = seq_info(a, seq);
     const int M = si.nq * p.G;
-    const int m0 = rb * 64;
+    const int m0 = rb * (NW * 32);
     if (m0 >= M) return;
 
     const int tid = threadIdx.x;
-    const int r = tid >> 2, part = tid & 3;
-    const int m = m0 + r;
+    const int wave = tid >> 6;
+    const int lane = tid & 63;
+    const int j = lane & 31;
+    const int hl = lane >> 5;
+    const int m = m0 + wave * 32 + j;
     const bool row_ok = m < M;
     const int qi = row_ok ? m / p.G : 0;
     const int head = kvh * p.G + (row_ok ? m - qi * p.G : 0);
+
+    // Q^T B operand: channel 2s + hl of the lane's row for step s, scaled.
+    float qf[KSF];
+    {
+        const float* qrow = (const float*)a.q + (int64_t)layer * a.q_stride[0] +
+                            (int64_t)(si.q0 + qi) * a.q_stride[1] + (int64_t)head * a.q_stride[2];
+#pragma unroll
+        for (int s = 0; s < KSF; ++s) qf[s] = row_ok ? qrow[2 * s + hl] * a.scale : 0.f;
+    }
     const int qpos = row_ok ? a.q_pos[si.q0 + qi] : -1;
     int row_start, row_end;
     visible_range(qpos, si.kvl, a.window, row_start, row_end);   // (0, 0) for rows past M
+    const int wmin = wave_min_i(row_ok ? row_end : 0x7fffffff);
     const int wmax = wave_max_i(row_end);
     const int wsmin = wave_min_i(row_ok ? row_start : 0x7fffffff);
-    if ((tid & 63) == 0) {
-        red[tid >> 6] = wmax;
-        red_start[tid >> 6] = wsmin;
+    const int wsmax = wave_max_i(row_start);
+    if (lane == 0) {
+        red[wave] = wmax;
+        red_min[wave] = wmin;
+        red_start[wave] = wsmin;
+        red_smax[wave] = wsmax;
     }
     __syncthreads();
-    const int loop_end = max(max(red[0], red[1]), max(red[2], red[3]));
-    const int s_min = min(min(red_start[0], red_start[1]), min(red_start[2], red_start[3]));
-    const int k_first = s_min == 0x7fffffff ? 0 : s_min / BN * BN;   // tiles before every window are skipped
-    const int k_begin = max(k_first, split * p.chunk);
-    const int k_end = min(loop_end, split * p.chunk + p.chunk);
+    const int e_max = max(red[0], red[1]);
+    const int s_min = min(red_start[0], red_start[1]);
+    const int split_begin = split * p.chunk;
+    const int k_begin = max(split_begin, s_min == 0x7fffffff ? 0 : s_min / BN * BN);   // tiles before every window are skipped
+    const int k_end = min(min(si.kvl, split_begin + p.chunk), e_max);
 
-    const float* qrow = (const float*)a.q + (int64_t)layer * a.q_stride[0] +
-                        (int64_t)(si.q0 + qi) * a.q_stride[1] + (int64_t)head * a.q_stride[2] + part * DQ;
-    float qv[DQ], ov[DQ];
-#pragma unroll
-    for (int c = 0; c < DQ; ++c) {
-        qv[c] = row_ok ? qrow[c] * a.scale : 0.f;
-        ov[c] = 0.f;
-    }
-    float m_run = -INFINITY, l_run = 0.f;
     const float* kbase = (const float*)a.k + (int64_t)layer * a.k_stride[0] + (int64_t)kvh * a.k_stride[1] +
                          si.base * a.k_stride[2];
     const float* vbase = (const float*)a.v + (int64_t)layer * a.v_stride[0] + (int64_t)kvh * a.v_stride[1] +
                          si.base * a.v_stride[2];
-    // Tile t+1 is loaded into registers while tile t is consumed from LDS.
-    constexpr int NL = BN * D / 4 / 256;   // 16-byte loads per thread per tensor
-    f32x4 pk[NL], pvv[NL];
-    auto load_tile = [&](int t0) {
+    // Thread tid moves 16-byte pieces tid + 128 i of each tensor's tile.  K:
+    // key (tid + 128 i) % 32, channels 4 ((tid + 128 i) / 32) .. +3 (consecutive
+    // threads write consecutive words of the transposed tile); V: key
+    // (tid + 128 i) / (D/4), channels 4 ((tid + 128 i) % (D/4)) .. +3.  Keys
+    // past k_end load zeros (their scores are masked, and 0 * 0 adds nothing).
+    f32x4 pk[NL], pv[NL];
+    auto load_tile = [&](int t0) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < NL; ++i) {
-            const int id = tid + i * 256, key = id / (D / 4), c = id % (D / 4);
-            const bool in = t0 + key < k_end;
-            pk[i] = in ? *(const f32x4*)(kbase + (int64_t)(t0 + key) * a.k_stride[2] + c * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
-            pvv[i] = in ? *(const f32x4*)(vbase + (int64_t)(t0 + key) * a.v_stride[2] + c * 4)
-                        : f32x4{0.f, 0.f, 0.f, 0.f};
+            const int id = tid + i * (NW * 64);
+            const int kk = id % BN, kc = id / BN, vk = id / (D / 4), vc = id % (D / 4);
+            pk[i] = t0 + kk < k_end ? *(const f32x4*)(kbase + (int64_t)(t0 + kk) * a.k_stride[2] + kc * 4)
+                                    : f32x4{0.f, 0.f, 0.f, 0.f};
+            pv[i] = t0 + vk < k_end ? *(const f32x4*)(vbase + (int64_t)(t0 + vk) * a.v_stride[2] + vc * 4)
+                                    : f32x4{0.f, 0.f, 0.f, 0.f};
         }
     };
+
+    f32x16 o[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[db] = f32x16{};
+    float m_run = -INFINITY, l_run = 0.f;   // running maximum (log2 units) and sum
     if (k_begin < k_end) load_tile(k_begin);
     for (int t0 = k_begin; t0 < k_end; t0 += BN) {
-        __syncthreads();
+        __syncthreads();   // every wave is done with the previous tile
 #pragma unroll
         for (int i = 0; i < NL; ++i) {
-            const int id = tid + i * 256, key = id / (D / 4), c = id % (D / 4);
-            *(f32x4*)(k_lds + key * D + c * 4) = pk[i];
-            *(f32x4*)(v_lds + key * D + c * 4) = pvv[i];
+            const int id = tid + i * (NW * 64);
+            const int kk = id % BN, kc = id / BN, vk = id / (D / 4), vc = id % (D / 4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) kt_lds[(kc * 4 + e) * BN + kk] = pk[i][e];
+            *(f32x4*)(v_lds + vk * D + vc * 4) = pv[i];
         }
         __syncthreads();
         if (t0 + BN < k_end) load_tile(t0 + BN);
-        // The tile's 32 scores first (independent dot products), then one
-        // online-softmax step for the whole tile: its maximum, one rescale of
-        // the running state, 32 independent exponentials and the PV sums.
-        const int n = min(BN, k_end - t0);
-        float sc[BN];
+
+        // S^T = K Q^T: step s takes channels 2s (lanes 0-31) and 2s + 1 (lanes 32-63).
+        f32x16 sc = f32x16{};
 #pragma unroll
-        for (int kk = 0; kk < BN; ++kk) {
-            float acc = 0.f;
+        for (int s = 0; s < KSF; ++s)
+            sc = __builtin_amdgcn_mfma_f32_32x32x2f32(kt_lds[(2 * s + hl) * BN + j], qf[s], sc, 0, 0, 0);
+        // Element r of the lane holds key t0 + 8 (r / 4) + 4 hl + r % 4 of row j.
+        float mx = -INFINITY;
 #pragma unroll
-            for (int c = 0; c < DQ; c += 4) {
-                const f32x4 kv = *(const f32x4*)(k_lds + kk * D + part * DQ + c);
-                acc = fmaf(qv[c], kv[0], acc);
-                acc = fmaf(qv[c + 1], kv[1], acc);
-                acc = fmaf(qv[c + 2], kv[2], acc);
-                acc = fmaf(qv[c + 3], kv[3], acc);
-            }
-            sc[kk] = acc;
+        for (int r = 0; r < 16; ++r) {
+            const int key = t0 + (r >> 2) * 8 + hl * 4 + (r & 3);
+            const float v = key < row_end && key >= row_start && key < k_end ? sc[r] * kLog2e : -INFINITY;
+            sc[r] = v;
+            mx = fmaxf(mx, v);
         }
-        float cmax = -INFINITY;
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        // Branch-free (the MFMAs below run for the whole wave): a row that has
+        // seen no visible key keeps o = 0 and l = 0 (alpha 0, probabilities 0).
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+        float lsum = 0.f;
 #pragma unroll
-        for (int kk = 0; kk < BN; ++kk) {
-            float v = sc[kk] + __shfl_xor(sc[kk], 1);
-            v += __shfl_xor(v, 2);
-            const int key = t0 + kk;
-            // invisible keys (uniform over a row's 4 lanes) drop out
-            v = kk < n && key < row_end && key >= row_start ? v : -INFINITY;
-            sc[kk] = v;
-            cmax = fmaxf(cmax, v);
+        for (int r = 0; r < 16; ++r) {
+            const float e = sc[r] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sc[r] - m_new);
+            sc[r] = e;
+            lsum += e;
         }
-        if (cmax != -INFINITY) {
-            const float m_new = fmaxf(m_run, cmax);
-            const float alpha = expf(m_run - m_new);   // 0 while the running maximum is -inf
-            float psum = 0.f;
+        l_run = l_run * alpha + lsum;
+        m_run = m_new;
 #pragma unroll
-            for (int kk = 0; kk < BN; ++kk) {
-                const float pe = sc[kk] == -INFINITY ? 0.f : expf(sc[kk] - m_new);
-                sc[kk] = pe;
-                psum += pe;
-            }
-            l_run = l_run * alpha + psum;
+        for (int db = 0; db < DB; ++db) {
+            o[db] *= alpha;
 #pragma unroll
-            for (int c = 0; c < DQ; c += 4) {
-                f32x4 acc = {ov[c] * alpha, ov[c + 1] * alpha, ov[c + 2] * alpha, ov[c + 3] * alpha};
+            for (int jj = 0; jj < 4; ++jj)
 #pragma unroll
-                for (int kk = 0; kk < BN; ++kk) {
-                    const f32x4 vv = *(const f32x4*)(v_lds + kk * D + part * DQ + c);
-                    acc[0] = fmaf(sc[kk], vv[0], acc[0]);
-                    acc[1] = fmaf(sc[kk], vv[1], acc[1]);
-                    acc[2] = fmaf(sc[kk], vv[2], acc[2]);
-                    acc[3] = fmaf(sc[kk], vv[3], acc[3]);
-                }
-                ov[c] = acc[0];
-                ov[c + 1] = acc[1];
-                ov[c + 2] = acc[2];
-                ov[c + 3] = acc[3];
-            }
-            m_run = m_new;
+                for (int rr = 0; rr < 4; ++rr)
+                    o[db] = __builtin_amdgcn_mfma_f32_32x32x2f32(v_lds[(8 * jj + 4 * hl + rr) * D + db * 32 + j],
+                                                                 sc[4 * jj + rr], o[db], 0, 0, 0);
         }
     }
+
+    // The two halves of a row hold disjoint keys.
+    const float l_tot = l_run + __shfl_xor(l_run, 32);
     if (!row_ok) return;
-    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const float lse2 = l_tot > 0.f ? m_run + __log2f(l_tot) : -INFINITY;
     const int64_t row = si.q0 + qi;
+    // Element 4 jj + rr of block db holds channel 32 db + 8 jj + 4 hl + rr of the row.
+    float* dst;
     if (p.splits == 1) {
-        float* orow = (float*)a.out + (int64_t)layer * a.o_stride[0] + row * a.o_stride[1] +
-                      (int64_t)head * a.o_stride[2] + part * DQ;
-#pragma unroll
-        for (int c = 0; c < DQ; ++c) orow[c] = ov[c] * inv;
-        if (a.lse_out && part == 0)
-            a.lse_out[((int64_t)layer * a.total_q + row) * a.n_heads + head] =
-                l_run > 0.f ? m_run + logf(l_run) : -INFINITY;
+        dst = (float*)a.out + (int64_t)layer * a.o_stride[0] + row * a.o_stride[1] + (int64_t)head * a.o_stride[2];
+        if (a.lse_out && hl == 0)
+            a.lse_out[((int64_t)layer * a.total_q + row) * a.n_heads + head] = lse2 * kLn2;
     } else {
         // split partial: normalised output and its log2-sum-exp (the combine's domain)
         const int64_t item = (((int64_t)split * a.n_layers + layer) * a.total_q + row) * a.n_heads + head;
-        float* wo = a.ws_o + item * D + part * DQ;
-#pragma unroll
-        for (int c = 0; c < DQ; ++c) wo[c] = ov[c] * inv;
-        if (part == 0) a.ws_lse[item] = l_run > 0.f ? (m_run + logf(l_run)) * kLog2e : -INFINITY;
+        dst = a.ws_o + item * D;
+        if (hl == 0) a.ws_lse[item] = lse2;
     }
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+            *(f32x4*)(dst + db * 32 + jj * 8 + hl * 4) =
+                f32x4{o[db][4 * jj] * inv, o[db][4 * jj + 1] * inv, o[db][4 * jj + 2] * inv, o[db][4 * jj + 3] * inv};
 }
 
 // Merge split-KV partials: out = sum_s w_s O_s / sum_s w_s with
@@ -366,9 +383,9 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
     hipError_t e;
     if (a.dtype == 1) {
         if (a.head_dim == 64)
-            hipLaunchKernelGGL((attn_gqa_f32<64>), grid, block, 0, stream, a, p);
+            hipLaunchKernelGGL((attn_gqa_f32<64>), grid, dim3(128), 0, stream, a, p);
         else
-            hipLaunchKernelGGL((attn_gqa_f32<128>), grid, block, 0, stream, a, p);
+            hipLaunchKernelGGL((attn_gqa_f32<128>), grid, dim3(128), 0, stream, a, p);
         e = hipGetLastError();
     } else {
         e = a.variant == 1 ? launch_attn_mla_bf16(a, p, grid, stream) : launch_attn_gqa_bf16(a, p, grid, stream);
