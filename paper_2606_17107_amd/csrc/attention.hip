@@ -82,9 +82,14 @@ __global__ __launch_bounds__(128) void attn_gqa_f32(AttnArgs a, Plan p) {
     __syncthreads();
     const int e_max = max(red[0], red[1]);
     const int s_min = min(red_start[0], red_start[1]);
-    const int split_begin = split * p.chunk;
-    const int k_begin = max(split_begin, s_min == 0x7fffffff ? 0 : s_min / BN * BN);   // tiles before every window are skipped
-    const int k_end = min(min(si.kvl, split_begin + p.chunk), e_max);
+    // Keys [lo, hi) hold every key a row of the workgroup sees (whole tiles
+    // from the first window start); the splits share them in equal runs of
+    // whole tiles.
+    const int lo = s_min == 0x7fffffff ? 0 : s_min / BN * BN;
+    const int hi = min(si.kvl, e_max);
+    const int run = hi > lo ? ((hi - lo + p.splits - 1) / p.splits + BN - 1) / BN * BN : 0;
+    const int k_begin = lo + split * run;
+    const int k_end = min(hi, k_begin + run);
 
     const float* kbase = (const float*)a.k + (int64_t)layer * a.k_stride[0] + (int64_t)kvh * a.k_stride[1] +
                          si.base * a.k_stride[2];
@@ -286,7 +291,6 @@ Plan make_plan(const AttnArgs& a, int splits) {
     Plan p;
     p.G = a.n_heads / a.n_kv_heads;
     const int64_t m_rows = (int64_t)a.max_q * p.G;
-    int tile = 32;
     if (a.variant == 1) {
         // MLA: four waves of 32 whole rows; 32-key tiles in 2 LDS stages.
         p.qb = 1;
@@ -305,9 +309,6 @@ Plan make_plan(const AttnArgs& a, int splits) {
     if (p.rbs < 1) p.rbs = 1;
     p.splits = splits;
     p.n_groups = a.n_layers * a.n_kv_heads * a.n_seqs * splits;
-    int chunk = (a.max_kv_len + splits - 1) / splits;
-    chunk = (chunk + tile - 1) / tile * tile;
-    p.chunk = chunk < tile ? tile : chunk;
     return p;
 }
 
@@ -339,11 +340,15 @@ int attention_splits(const AttnArgs& a) {
     // least 512 keys per split, at most 32 splits.
     const Plan p = make_plan(a, 1);
     const int64_t wgs = (int64_t)p.n_groups * p.rbs;   // workgroups per split
+    // Keys one workgroup's rows see: with a sliding window, about the window
+    // plus the span of the queries (contiguous suffix positions).
+    const int64_t kv = a.window > 0 && (int64_t)a.window + a.max_q < a.max_kv_len ? (int64_t)a.window + a.max_q
+                                                                                  : a.max_kv_len;
     if (a.dtype == 1) {
         // fp32 path (small problems): one workgroup per CU, at least 64 keys
         // per split, at most 32 splits.
         int64_t s = (kCUs + wgs - 1) / wgs;
-        const int64_t max_s = a.max_kv_len / 64;
+        const int64_t max_s = kv / 64;
         if (s > max_s) s = max_s;
         if (s > 32) s = 32;
         return s < 1 ? 1 : (int)s;
@@ -351,12 +356,12 @@ int attention_splits(const AttnArgs& a) {
     const int64_t slots = kCUs * (int64_t)wgs_per_cu(a, p);
     const double rate = a.variant == 1 ? 1.1e15 : 1.0e15;
     const double slot_rate = rate / (double)slots;
-    const double wg_flops = (double)p.BM * a.max_kv_len * (a.head_dim + a.head_dim_v) * 2.0;
+    const double wg_flops = (double)p.BM * kv * (a.head_dim + a.head_dim_v) * 2.0;
     const double comb_bytes = (double)a.n_layers * a.total_q * a.n_heads * (a.head_dim_v + 1) * 4.0 * 2.0;
     int best = 1;
     double best_t = 1e30;
     for (int s = 1; s <= 32; ++s) {
-        if (s > 1 && a.max_kv_len / s < 512) break;
+        if (s > 1 && kv / s < 512) break;
         const double rounds = (double)((wgs * s + slots - 1) / slots);
         const double t = rounds * (20e-6 + (wg_flops / s) / slot_rate) + (s > 1 ? s * comb_bytes / 5e12 + 5e-6 : 0.0);
         if (t < best_t * (1.0 - 1e-9)) {

@@ -32,8 +32,7 @@ struct Plan {
     int BM;         // rows per workgroup
     int rbs;        // row blocks per group
     int n_groups;   // layers x kv heads x sequences x splits
-    int splits;
-    int chunk;      // keys per split (multiple of the key tile)
+    int splits;     // each workgroup's key range is shared by this many splits in equal runs of whole tiles
     int qb, nw, ns; // bf16 GQA kernel shape: 32-row blocks per wave, waves, LDS stages
 };
 

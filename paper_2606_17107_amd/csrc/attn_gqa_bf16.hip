@@ -157,10 +157,14 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_gqa_bf16_kernel(AttnArgs 
         s_max = max(s_max, red_smax[w]);
     }
 
-    // Tiles wholly before every row's window start are skipped.
-    const int split_begin = split * p.chunk;
-    const int k_begin = max(split_begin, s_min == 0x7fffffff ? 0 : s_min / BN * BN);
-    const int loop_end = min(min(si.kvl, split_begin + p.chunk), e_max);
+    // Keys [lo, hi) hold every key a row of the workgroup sees (whole tiles
+    // from the first window start; tiles wholly before every window are
+    // skipped); the splits share them in equal runs of whole tiles.
+    const int lo = s_min == 0x7fffffff ? 0 : s_min / BN * BN;
+    const int hi = min(si.kvl, e_max);
+    const int run = hi > lo ? ((hi - lo + p.splits - 1) / p.splits + BN - 1) / BN * BN : 0;
+    const int k_begin = lo + split * run;
+    const int loop_end = min(hi, k_begin + run);
     const int n_tiles = loop_end > k_begin ? (loop_end - k_begin + BN - 1) / BN : 0;
 
     const uint16_t* kbase = (const uint16_t*)a.k + (int64_t)layer * a.k_stride[0] +

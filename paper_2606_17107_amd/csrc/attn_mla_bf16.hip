@@ -138,10 +138,14 @@ __global__ __launch_bounds__(kMlaWaves * 64, 1) void attn_mla_bf16_kernel(AttnAr
         e_max = max(e_max, red[w]);
         s_min = min(s_min, red_start[w]);
     }
-    // Tiles wholly before every row's window start are skipped.
-    const int split_begin = split * p.chunk;
-    const int k_begin = max(split_begin, s_min == 0x7fffffff ? 0 : s_min / MBN * MBN);
-    const int loop_end = min(min(si.kvl, split_begin + p.chunk), e_max);
+    // Keys [lo, hi) hold every key a row of the workgroup sees (whole tiles
+    // from the first window start); the splits share them in equal runs of
+    // whole tiles.
+    const int lo = s_min == 0x7fffffff ? 0 : s_min / MBN * MBN;
+    const int hi = min(si.kvl, e_max);
+    const int run = hi > lo ? ((hi - lo + p.splits - 1) / p.splits + MBN - 1) / MBN * MBN : 0;
+    const int k_begin = lo + split * run;
+    const int loop_end = min(hi, k_begin + run);
     const int n_tiles = loop_end > k_begin ? (loop_end - k_begin + MBN - 1) / MBN : 0;
 
     const uint16_t* kbase = (const uint16_t*)a.k + (int64_t)layer * a.k_stride[0] + si.base * a.k_stride[2];
