@@ -292,11 +292,11 @@ def test_paged_mla_page_strides_must_match():
     assert st == pkv.PKV_ERR_SHAPE and "v_block_table" in pkv.pkv_last_error()
 
 
-def planned_splits(L, H, Hkv, d, dv, total_q, kv, variant=0, dtype=0):
+def planned_splits(L, H, Hkv, d, dv, total_q, kv, variant=0, dtype=0, window=0):
     """Split count the library picks, read back through the workspace size."""
     d_ = pkv.pkv_attn_desc()
     d_.dtype, d_.variant, d_.n_layers, d_.n_seqs, d_.head_dim_v = dtype, variant, L, 1, dv
-    d_.total_q, d_.max_q, d_.max_kv_len, d_.n_splits, d_.window = total_q, total_q, kv, 0, 0
+    d_.total_q, d_.max_q, d_.max_kv_len, d_.n_splits, d_.window = total_q, total_q, kv, 0, window
     d_.cache_slots = kv
     d_.q_stride = pkv._i64x3(total_q * H * d, H * d, d)
     d_.k_stride = d_.v_stride = pkv._i64x3(Hkv * kv * d, kv * d, d)
@@ -322,6 +322,17 @@ def test_split_planner_choices():
     assert planned_splits(1, 8, 2, 128, 128, 16, 300) == 1
     assert planned_splits(1, 8, 2, 128, 128, 16, 1000) == 1    # under 2 x 512 keys: no split
     assert planned_splits(1, 8, 2, 128, 128, 16, 4096) > 1     # one layer, one KV head pair: split to fill CUs
+
+
+def test_split_planner_sizes_windowed_work_by_the_window():
+    """With a sliding window a workgroup sees about window + queries keys, not the whole cache: the
+    32k prefill with a 4096-key window runs unsplit (its rounds already fill the CUs; 1.67 ms against
+    1.94 ms split 2 ways on MI355X), one 8B layer splits by its window (2 ways for 1024 keys, 8 for
+    4096, 16 without a window)."""
+    assert planned_splits(28, 28, 4, 128, 128, 1024, 50176, window=4096) == 1
+    assert planned_splits(1, 32, 8, 128, 128, 64, 8256, window=1024) == 2
+    assert planned_splits(1, 32, 8, 128, 128, 64, 8256, window=4096) == 8
+    assert planned_splits(1, 32, 8, 128, 128, 64, 8256, window=10000) == 16   # window past the cache
 
 
 def test_split_planner_fp32():
