@@ -7,6 +7,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 import torch
 
@@ -352,3 +353,50 @@ def test_stream_copy_library_exports():
     assert os.path.exists(B.COPY_LIB)
     lib = ctypes.CDLL(B.COPY_LIB)
     assert hasattr(lib, "pkv_stream_copy")
+
+
+def test_workspace_size_over_random_descriptors():
+    """The split planner over 3000 seeded descriptors (layer, head, length, window and split counts of
+    every size the ABI accepts, plus invalid ones): the size is 0 for an invalid descriptor or an
+    unsplit plan, otherwise a whole number of per-split records: 2..32 splits of the library's own
+    choice, and an explicit split count kept unless it exceeds ceil(max_kv_len / 64).  Host code
+    only: nothing launches."""
+    rng = np.random.default_rng(2024)
+    for _ in range(3000):
+        variant = int(rng.integers(0, 2))
+        dtype = 0 if variant else int(rng.integers(0, 2))
+        if variant:
+            Hkv, H, D, dv = 1, int(rng.choice([8, 16, 128])), 576, 512
+        else:
+            Hkv = int(rng.choice([1, 2, 4, 8]))
+            H = Hkv * int(rng.choice([1, 3, 4, 7, 8]))
+            D = int(rng.choice([64, 128, 96]))   # 96 is unsupported
+            dv = D
+        L, n_seqs = int(rng.integers(1, 65)), int(rng.integers(1, 9))
+        total_q = int(rng.integers(0, 4097))
+        max_q = int(rng.integers(0, total_q + 1)) if n_seqs > 1 else total_q
+        kv = int(rng.integers(0, 1 << 17))
+        splits = int(rng.choice([0, 0, 1, 2, 3, 16, 33]))
+        window = int(rng.choice([0, 0, 1, 100, 4096, 1 << 20]))
+        d_ = pkv.pkv_attn_desc()
+        d_.dtype, d_.variant, d_.n_layers, d_.n_seqs, d_.head_dim_v = dtype, variant, L, n_seqs, dv
+        d_.total_q, d_.max_q, d_.max_kv_len, d_.n_splits, d_.window = total_q, max_q, kv, splits, window
+        d_.cu_q = BASE + (1 << 33) if n_seqs > 1 else None
+        d_.cache_slots = kv
+        d_.q_stride = pkv._i64x3(max(total_q, 1) * H * D, H * D, D)
+        d_.k_stride = d_.v_stride = pkv._i64x3(Hkv * max(kv, 1) * D, max(kv, 1) * D, D)
+        d_.o_stride = pkv._i64x3(max(total_q, 1) * H * dv, H * dv, dv)
+        n = pkv.pkv_attention_workspace_size(d_, H, Hkv, D)
+        valid = D != 96
+        if not valid:
+            assert n == 0
+            continue
+        per_split = L * total_q * H * (dv + 1) * 4
+        if n == 0:
+            continue
+        assert per_split > 0 and n % per_split == 0, (n, per_split)
+        s = n // per_split
+        if splits > 1:
+            assert s == min(splits, (kv + 63) // 64), (s, splits, kv)   # explicit: kept, or lowered
+        else:
+            assert splits == 0 and 2 <= s <= 32, (s, splits)           # the library's own choice
